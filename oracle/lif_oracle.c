@@ -53,7 +53,10 @@ static double surrogate(double alpha, double u)
  *   hard:  dv^{t+1}/dv^t = k (1 - y^t) + (V_rest - k v^t) delta^t
  *          (= k [1 - y^t - v^t delta^t] at V_rest = 0, Eq. (3) as printed),
  *   soft:  dv^{t+1}/dv^t = k (1 - V_th delta^t).
- * dL/dv^{T+1} = g_next (0 for the last layer of time). */
+ * dL/dv^{T+1} = g_next (0 for the last layer of time).
+ * The bound gx_mag runs the same recurrence with every term in absolute value (each term
+ * of dv^{t+1}/dv^t separately), so it bounds the rounding error of any evaluation of
+ * Eq. (3) that rounds each term with a small relative error, even where terms cancel. */
 void lif_oracle_backward(const lif_oracle_params *p, int64_t T, int64_t N, const float *v,
                          const uint8_t *y, const double *gy, const double *gy_mag,
                          const double *g_next, double *gx, double *gx_mag)
@@ -66,13 +69,16 @@ void lif_oracle_backward(const lif_oracle_params *p, int64_t T, int64_t N, const
             const int64_t i = t * N + n;
             const double vt = v[i];
             const double d = surrogate(alpha, vt - th);
-            double dv_next;
-            if (p->soft_reset)
+            double dv_next, dv_next_mag;
+            if (p->soft_reset) {
                 dv_next = k * (1.0 - th * d);
-            else
+                dv_next_mag = k * (1.0 + fabs(th) * d);
+            } else {
                 dv_next = k * (1.0 - (double)y[i]) + (rest - k * vt) * d;
+                dv_next_mag = k * (1.0 - (double)y[i]) + fabs(rest - k * vt) * d;
+            }
             const double g = gy[i] * d + dv_next * g_after;
-            const double m = gy_mag[i] * d + fabs(dv_next) * m_after;
+            const double m = gy_mag[i] * d + dv_next_mag * m_after;
             gx[i] = g;
             gx_mag[i] = m;
             g_after = g;

@@ -15,8 +15,8 @@
  * operation (built with -ffp-contract=off: no fused multiply-add).  It has to:
  * the membrane decides an integer (the spike), and that decision is taken in
  * the GPU kernel's precision.  The backward runs in fp64 on the fp32 membrane
- * trajectory and also returns a magnitude bound (the same recurrence on
- * absolute values) that scales the comparison tolerance.
+ * trajectory and also returns a magnitude bound (the same recurrence with every
+ * term in absolute value) that scales the comparison tolerance.
  *
  * Pins (tests/test_oracle_pins.py): constant-input spike periods (hard reset,
  * and soft reset at k = 1), the T = 1 Heaviside, the geometric leak below
