@@ -1,0 +1,128 @@
+/*
+ * snn_lif.h -- C ABI of the temporally fused LIF spiking-neuron layer for MI355X (gfx950).
+ *
+ * What it computes (Li et al., "Towards Scalable GPU-Accelerated SNN Training via
+ * Temporal Fusion"):
+ *   forward  -- for every neuron, all T time steps of the iterative LIF model in one
+ *               kernel (temporal fusion, Sec. 3.2): the membrane update of Sec. 3.1
+ *               Eq. (1) (leak, input integration, reset) and the Heaviside spike of
+ *               Eq. (2), with H(0) = 1;
+ *   backward -- the surrogate-gradient recurrence of Eq. (3), run in reverse time in one
+ *               kernel, with the sigmoid surrogate of Sec. 5.2 evaluated at v - V_th.
+ *
+ * Conventions shared by every entry point:
+ *   - Tensors are dense and time-major, [T][N]: row t (the paper's step t+1) starts at
+ *     element t*N.  A per-step shape such as [B][C][H][W] is contiguous, so N = B*C*H*W.
+ *   - Every data pointer is a DEVICE pointer owned by the caller and 16-byte aligned.
+ *   - The library never allocates, never synchronizes, keeps no pointer after it returns
+ *     and has no mutable global state: calls are re-entrant and thread-safe.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL = null stream)
+ *     and runs asynchronously with respect to the host.
+ *   - Arguments are validated before anything is launched.  On error nothing is written
+ *     and a negative snn_status is returned; a rejected launch returns SNN_E_LAUNCH.
+ *     Faults inside a kernel surface at the caller's next synchronization.
+ *   - T == 0 or N == 0 is an empty problem: SNN_OK, nothing is launched and the data
+ *     pointers are not used (they may be NULL).
+ *   - Limits: 0 <= T <= 2^31 - 1, 0 <= N <= 2^31, T * N <= 2^44 (SNN_E_SHAPE beyond).
+ */
+#ifndef SNN_LIF_H
+#define SNN_LIF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    SNN_OK = 0,
+    SNN_E_NULL = -1,        /* a required pointer is NULL */
+    SNN_E_SHAPE = -2,       /* negative or too large T, N, B, F */
+    SNN_E_PARAM = -3,       /* a hyper-parameter or enum value out of range */
+    SNN_E_ALIGN = -4,       /* a data pointer is not 16-byte aligned */
+    SNN_E_UNSUPPORTED = -5, /* a combination this build does not implement */
+    SNN_E_LAUNCH = -6       /* the HIP runtime rejected the kernel launch */
+} snn_status;
+
+typedef enum {
+    SNN_RESET_HARD = 0, /* Eq. (1): after a spike the membrane restarts at V_rest (+ input) */
+    SNN_RESET_SOFT = 1  /* not in the paper: subtract V_th, then leak:
+                           v^t = k (v^{t-1} - V_th y^{t-1}) + x^t; backward factor k (1 - V_th delta) */
+} snn_reset;
+
+typedef enum {
+    SNN_IO_F32 = 0,  /* x, dL/dy and dL/dx are float32 */
+    SNN_IO_BF16 = 1  /* bfloat16 bit patterns (uint16); widened exactly, membrane kept in fp32,
+                        dL/dx rounded to nearest even when stored */
+} snn_io;
+
+typedef enum {
+    SNN_SPK_U8 = 0,  /* one byte per neuron (0 or 1): row t at byte t*N */
+    SNN_SPK_BITS = 1 /* one bit per neuron: neuron n of row t is bit (n & 7) of byte
+                        t*row_bytes + (n >> 3), row_bytes = 8*ceil(N/64) (whole little-endian
+                        64-bit words), padding bits are written as 0 */
+} snn_spk;
+
+typedef struct {
+    float decay;   /* k_tau of Eq. (1), in [0, 1]; the paper relates it to tau as k = 1 - 1/tau */
+    float v_th;    /* V_th of Eq. (2), finite */
+    float v_reset; /* V_rest of Eq. (1): membrane before step 1 and the hard-reset value, finite */
+    float alpha;   /* surrogate sharpness (Sec. 5.2): delta(u) = alpha e^{-alpha u}/(1+e^{-alpha u})^2,
+                      > 0 and finite */
+    int32_t reset; /* snn_reset */
+    int32_t io;    /* snn_io */
+    int32_t spk;   /* snn_spk */
+} snn_lif_cfg;
+
+/* Bytes of one spike row for N neurons in cfg->spk's format (N, or 8*ceil(N/64)).
+ * Host-only; SNN_E_NULL / SNN_E_PARAM / SNN_E_SHAPE on bad arguments. */
+snn_status snn_spike_row_bytes(const snn_lif_cfg *cfg, int64_t N, size_t *bytes);
+
+/* Bytes of the forward-to-backward state for a [T][N] layer.  The content is opaque
+ * (fp32 membrane checkpoints at fixed step intervals; 0 bytes when T is short enough that
+ * the backward recomputes the whole trajectory from x).  Host-only. */
+snn_status snn_lif_saved_bytes(const snn_lif_cfg *cfg, int64_t T, int64_t N, size_t *bytes);
+
+/* Forward of one LIF layer over all T steps (Eqs. (1), (2); temporal fusion, Sec. 3.2).
+ *   x       [T][N] in cfg->io dtype: input current x_i^(t).
+ *   spikes  [T][row_bytes] out: y_i^(t) in cfg->spk format.
+ *   saved   snn_lif_saved_bytes() bytes out (may be NULL when that size is 0).
+ *   v_out   NULLABLE [T][N] float32 out: membrane after input integration, before any
+ *           reset (the v_i^(t) of Eq. (1)).  Meant for tests; pass NULL otherwise.
+ * x, spikes and saved must not be modified between this call and the matching backward. */
+snn_status snn_lif_forward(const snn_lif_cfg *cfg, int64_t T, int64_t N, const void *x,
+                           void *spikes, void *saved, float *v_out, void *stream);
+
+/* Backward of the same layer (Eq. (3), reverse time, surrogate of Sec. 5.2).
+ *   x, saved  exactly as passed to / written by snn_lif_forward with the same cfg, T, N.
+ *   grad_s    [T][N] in cfg->io dtype: dL/dy_i^(t).
+ *   grad_x    [T][N] in cfg->io dtype out: dL/dx_i^(t) (= dL/dv_i^(t)).  May be the same
+ *             buffer as grad_s (in place); any other overlap is undefined.
+ * The membrane trajectory is recomputed from x and the checkpoints, bit-identical to the
+ * forward's.  Only grad_x is produced: k_tau, V_th, V_rest get no gradient. */
+snn_status snn_lif_backward(const snn_lif_cfg *cfg, int64_t T, int64_t N, const void *x,
+                            const void *saved, const void *grad_s, void *grad_x, void *stream);
+
+/* Stand-in for the ANN operator between stacked LIF layers (not part of the paper's
+ * method): a per-feature gain, N = B*F neurons per step, neuron (b, f) at b*F + f.
+ *   forward:  x_next[t][b][f] = gain[f] * y[t][b][f]   (spikes in cfg->spk format,
+ *             x_next in cfg->io dtype, product in fp32 then rounded to the io dtype);
+ *   backward: grad_s[t][b][f] = gain[f] * grad_x_next[t][b][f]   (io dtype in and out;
+ *             may be the same buffer).
+ * gain is a device float32 [F] array. */
+snn_status snn_gain_spikes_forward(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
+                                   const void *spikes, const float *gain, void *x_next,
+                                   void *stream);
+snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
+                                  const void *grad_x_next, const float *gain, void *grad_s,
+                                  void *stream);
+
+/* Static text for a status code. */
+const char *snn_status_str(snn_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNN_LIF_H */

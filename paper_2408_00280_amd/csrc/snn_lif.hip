@@ -1,0 +1,710 @@
+// Temporally fused LIF layer for MI355X (gfx950): forward and backward kernels and the
+// C ABI declared in include/snn_lif.h.
+//
+// Design (see the header for the operation itself):
+//  * Neurons are independent (Sec. 3.1), so each lane owns V consecutive neurons and walks
+//    all T steps with their membranes in VGPRs (temporal fusion, Sec. 3.2).  Rows of the
+//    time-major [T][N] tensors are read and written coalesced along N, 16 bytes per lane
+//    (V = 4 fp32 or V = 8 bf16 neurons) when N is a multiple of V; otherwise V = 1.
+//  * Time is processed in chunks of K steps.  All K input rows of a chunk are loaded before
+//    the first step of the chunk is computed (they do not depend on the recurrence), so
+//    every lane keeps K loads in flight.
+//  * The forward saves no membrane for the backward except one fp32 checkpoint per neuron at
+//    the end of every chunk but the last.  The backward walks the chunks in reverse: it
+//    reloads the chunk's inputs, recomputes the chunk's membranes into VGPRs from the
+//    checkpoint with the same instruction sequence as the forward (bit-identical), then
+//    runs the reverse-time surrogate recurrence of Eq. (3) over the chunk.
+//  * The membrane update is one IEEE multiply and one IEEE add (no fused multiply-add:
+//    this file is compiled with -ffp-contract=off), so results are reproducible
+//    bit for bit.  The backward uses fused multiply-adds where it wants them, explicitly.
+//  * No MFMA: the work is elementwise across neurons and a scalar recurrence in time.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdint>
+#include <tuple>
+#include <utility>
+
+#include "snn_lif.h"
+
+namespace {
+
+constexpr int kBlock = 256;  // 4 wave64 per workgroup
+constexpr int kWave = 64;
+
+constexpr int64_t kMaxT = INT32_MAX;
+constexpr int64_t kMaxN = int64_t(1) << 31;
+constexpr int64_t kMaxTN = int64_t(1) << 44;
+
+// Kernel-side hyper-parameters.
+struct LifK {
+    float k;      // decay k_tau
+    float th;     // V_th
+    float rest;   // V_rest
+    float alpha;  // surrogate sharpness
+    float c_exp;  // -alpha * log2(e): e^{-alpha |u|} = 2^{c_exp |u|}
+    float kth;    // k * V_th (soft-reset backward)
+};
+
+// ------------------------------------------------------------------------------------
+// Vectors of V consecutive neurons in the I/O dtype.
+template <int IO, int V>
+struct IoVec;
+
+template <>
+struct IoVec<SNN_IO_F32, 4> {
+    using raw = float4;
+    __device__ static raw load(const void* b, int64_t i) {
+        return *reinterpret_cast<const float4*>(static_cast<const float*>(b) + i);
+    }
+    __device__ static float get(const raw& r, int j) {
+        return j == 0 ? r.x : j == 1 ? r.y : j == 2 ? r.z : r.w;
+    }
+    __device__ static void store(void* b, int64_t i, const float (&f)[4]) {
+        *reinterpret_cast<float4*>(static_cast<float*>(b) + i) = make_float4(f[0], f[1], f[2], f[3]);
+    }
+};
+
+template <>
+struct IoVec<SNN_IO_F32, 1> {
+    using raw = float;
+    __device__ static raw load(const void* b, int64_t i) { return static_cast<const float*>(b)[i]; }
+    __device__ static float get(const raw& r, int) { return r; }
+    __device__ static void store(void* b, int64_t i, const float (&f)[1]) {
+        static_cast<float*>(b)[i] = f[0];
+    }
+};
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even) packed low/high in one dword.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+template <>
+struct IoVec<SNN_IO_BF16, 8> {
+    using raw = uint4;
+    __device__ static raw load(const void* b, int64_t i) {
+        return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(b) + i);
+    }
+    __device__ static float get(const raw& r, int j) {
+        const uint32_t w = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
+        return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+    }
+    __device__ static void store(void* b, int64_t i, const float (&f)[8]) {
+        uint4 w;
+        w.x = pack_bf16x2(f[0], f[1]);
+        w.y = pack_bf16x2(f[2], f[3]);
+        w.z = pack_bf16x2(f[4], f[5]);
+        w.w = pack_bf16x2(f[6], f[7]);
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(b) + i) = w;
+    }
+};
+
+template <>
+struct IoVec<SNN_IO_BF16, 4> {
+    using raw = uint2;
+    __device__ static raw load(const void* b, int64_t i) {
+        return *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(b) + i);
+    }
+    __device__ static float get(const raw& r, int j) {
+        const uint32_t w = (j >> 1) == 0 ? r.x : r.y;
+        return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+    }
+    __device__ static void store(void* b, int64_t i, const float (&f)[4]) {
+        uint2 w;
+        w.x = pack_bf16x2(f[0], f[1]);
+        w.y = pack_bf16x2(f[2], f[3]);
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(b) + i) = w;
+    }
+};
+
+template <>
+struct IoVec<SNN_IO_BF16, 1> {
+    using raw = uint32_t;
+    __device__ static raw load(const void* b, int64_t i) { return static_cast<const uint16_t*>(b)[i]; }
+    __device__ static float get(const raw& r, int) { return __uint_as_float(r << 16); }
+    __device__ static void store(void* b, int64_t i, const float (&f)[1]) {
+        static_cast<uint16_t*>(b)[i] = static_cast<uint16_t>(pack_bf16x2(f[0], 0.0f) & 0xffffu);
+    }
+};
+
+// ------------------------------------------------------------------------------------
+// One step of Eq. (1) then Eq. (2) for one neuron.  `y` is the previous step's spike on
+// entry and this step's on exit; `v` likewise for the membrane.
+template <int RESET>
+__device__ __forceinline__ void lif_step(const LifK& c, float& v, bool& y, float x) {
+#pragma clang fp contract(off)
+    if (RESET == SNN_RESET_HARD) {
+        v = y ? c.rest + x : c.k * v + x;
+    } else {
+        const float w = y ? v - c.th : v;
+        v = c.k * w + x;
+    }
+    y = v >= c.th;  // H(v - V_th) with H(0) = 1; NaN never fires
+}
+
+// Derivative of sigmoid(alpha u): alpha e / (1 + e)^2 with e = e^{-alpha |u|} (even in u).
+__device__ __forceinline__ float surrogate(const LifK& c, float u) {
+    const float e = __builtin_amdgcn_exp2f(c.c_exp * fabsf(u));
+    const float r = __builtin_amdgcn_rcpf(1.0f + e);
+    return (c.alpha * e) * (r * r);
+}
+
+// ------------------------------------------------------------------------------------
+// Spike rows.  `t` is the row; lanes own neurons [n0, n0 + V).
+template <int SPK, int V>
+struct SpikeOut;
+
+template <>
+struct SpikeOut<SNN_SPK_U8, 4> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[4]) {
+        const uint32_t w = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) |
+                           (uint32_t(y[3]) << 24);
+        if (active) *reinterpret_cast<uint32_t*>(s + t * row_bytes + n0) = w;
+    }
+};
+
+template <>
+struct SpikeOut<SNN_SPK_U8, 8> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[8]) {
+        uint2 w;
+        w.x = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) | (uint32_t(y[3]) << 24);
+        w.y = uint32_t(y[4]) | (uint32_t(y[5]) << 8) | (uint32_t(y[6]) << 16) | (uint32_t(y[7]) << 24);
+        if (active) *reinterpret_cast<uint2*>(s + t * row_bytes + n0) = w;
+    }
+};
+
+template <>
+struct SpikeOut<SNN_SPK_U8, 1> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[1]) {
+        if (active) s[t * row_bytes + n0] = uint8_t(y[0]);
+    }
+};
+
+// Bits, 4 neurons per lane: lanes 2j and 2j+1 share a byte; the odd lane's nibble is
+// moved to the even lane with a DPP quad permutation [1,0,3,2].  Every lane of the wave
+// must execute this (no divergence around it).
+template <>
+struct SpikeOut<SNN_SPK_BITS, 4> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[4]) {
+        int nib = active ? (int(y[0]) | (int(y[1]) << 1) | (int(y[2]) << 2) | (int(y[3]) << 3)) : 0;
+        const int other = __builtin_amdgcn_mov_dpp(nib, 0xB1, 0xF, 0xF, false);
+        if (((n0 >> 2) & 1) == 0 && n0 < row_bytes * 8)
+            s[t * row_bytes + (n0 >> 3)] = uint8_t(nib | (other << 4));
+    }
+};
+
+template <>
+struct SpikeOut<SNN_SPK_BITS, 8> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[8]) {
+        uint32_t b = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) b |= uint32_t(y[j]) << j;
+        if (n0 < row_bytes * 8) s[t * row_bytes + (n0 >> 3)] = uint8_t(active ? b : 0u);
+    }
+};
+
+// Bits, 1 neuron per lane: one wave64 ballot is one 64-bit word of the row.
+template <>
+struct SpikeOut<SNN_SPK_BITS, 1> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[1]) {
+        const uint64_t word = __ballot(active && y[0]);
+        if ((threadIdx.x & (kWave - 1)) == 0 && n0 < row_bytes * 8)
+            *reinterpret_cast<uint64_t*>(s + t * row_bytes + (n0 >> 3)) = word;
+    }
+};
+
+
+// ------------------------------------------------------------------------------------
+// fp32 rows of V neurons (checkpoints and the optional membrane output).
+template <int V>
+__device__ __forceinline__ void store_f32(float* p, const float (&f)[V]) {
+    if constexpr (V % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q)
+            reinterpret_cast<float4*>(p)[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
+    } else {
+#pragma unroll
+        for (int j = 0; j < V; ++j) p[j] = f[j];
+    }
+}
+
+template <int V>
+__device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
+    if constexpr (V % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < V / 4; ++q) {
+            const float4 a = reinterpret_cast<const float4*>(p)[q];
+            f[4 * q] = a.x;
+            f[4 * q + 1] = a.y;
+            f[4 * q + 2] = a.z;
+            f[4 * q + 3] = a.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < V; ++j) f[j] = p[j];
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Forward: one chunk of up to K steps.  FULL chunks skip the per-step bound test.
+template <int IO, int SPK, int RESET, int V, int K, bool FULL>
+__device__ __forceinline__ void forward_chunk(const LifK& c, int64_t N, int64_t t0, int kn, int64_t n0,
+                                              bool active, const void* __restrict__ x,
+                                              uint8_t* __restrict__ spikes, int64_t row_bytes,
+                                              float* __restrict__ v_out, float (&v)[V], bool (&y)[V]) {
+    using Io = IoVec<IO, V>;
+    typename Io::raw xr[K];
+    if (active) {
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            if (FULL || i < kn) xr[i] = Io::load(x, (t0 + i) * N + n0);
+    }
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        if (FULL || i < kn) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], active ? Io::get(xr[i], j) : 0.0f);
+            SpikeOut<SPK, V>::store(spikes, row_bytes, t0 + i, n0, active, y);
+            if (v_out != nullptr && active) store_f32<V>(v_out + (t0 + i) * N + n0, v);
+        }
+    }
+}
+
+// Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
+// N load nothing and report no spikes; they exist only to complete spike-bit words.
+template <int IO, int SPK, int RESET, int V, int K>
+__global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
+                                                             const void* __restrict__ x,
+                                                             uint8_t* __restrict__ spikes,
+                                                             int64_t row_bytes,
+                                                             float* __restrict__ saved,
+                                                             float* __restrict__ v_out) {
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const bool active = n0 < N;
+    float v[V];
+    bool y[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        v[j] = c.rest;  // v^0 = V_rest
+        y[j] = false;   // no spike before the first step
+    }
+    const int64_t n_chunks = (T + K - 1) / K;
+    for (int64_t ch = 0; ch < n_chunks; ++ch) {
+        const int64_t t0 = ch * K;
+        const int kn = int(T - t0 < K ? T - t0 : K);
+        if (kn == K)
+            forward_chunk<IO, SPK, RESET, V, K, true>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
+        else
+            forward_chunk<IO, SPK, RESET, V, K, false>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
+        if (ch + 1 < n_chunks && active) store_f32<V>(saved + ch * N + n0, v);
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Backward: one chunk.  v/y enter as the state before the chunk's first step; g enters as
+// dL/dv of the step after the chunk and leaves as dL/dv of the chunk's first step.
+template <int IO, int RESET, int V, int K, bool FULL>
+__device__ __forceinline__ void backward_chunk(const LifK& c, int64_t N, int64_t t0, int kn, int64_t n0,
+                                               const void* __restrict__ x, const void* gs, void* gx,
+                                               float (&v)[V], bool (&y)[V], float (&g)[V]) {
+    using Io = IoVec<IO, V>;
+    typename Io::raw xr[K];
+    typename Io::raw gr[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+        if (FULL || i < kn) xr[i] = Io::load(x, (t0 + i) * N + n0);
+    // dL/dy rows are consumed last-first: issue them in that order
+#pragma unroll
+    for (int i = K - 1; i >= 0; --i)
+        if (FULL || i < kn) gr[i] = Io::load(gs, (t0 + i) * N + n0);
+
+    // recompute the chunk's membranes, bit-identical to the forward
+    float vs[K][V];
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        if (FULL || i < kn) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                lif_step<RESET>(c, v[j], y[j], Io::get(xr[i], j));
+                vs[i][j] = v[j];
+            }
+        }
+    }
+
+    // Eq. (3) in reverse time: g^t = dL/dy^t delta^t + (dv^{t+1}/dv^t) g^{t+1}
+#pragma unroll
+    for (int i = K - 1; i >= 0; --i) {
+        if (FULL || i < kn) {
+            float out[V];
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                const float vt = vs[i][j];
+                const float d = surrogate(c, vt - c.th);
+                float dv_next;
+                if (RESET == SNN_RESET_HARD)  // k (1 - y^t) + (V_rest - k v^t) delta^t
+                    dv_next = fmaf(fmaf(-c.k, vt, c.rest), d, vt >= c.th ? 0.0f : c.k);
+                else                          // k (1 - V_th delta^t)
+                    dv_next = fmaf(-c.kth, d, c.k);
+                g[j] = fmaf(Io::get(gr[i], j), d, dv_next * g[j]);
+                out[j] = g[j];
+            }
+            Io::store(gx, (t0 + i) * N + n0, out);
+        }
+    }
+}
+
+template <int IO, int RESET, int V, int K>
+__global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
+                                                              const void* __restrict__ x,
+                                                              const float* __restrict__ saved,
+                                                              const void* gs, void* gx) {
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    if (n0 >= N) return;
+    float g[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
+    const int64_t n_chunks = (T + K - 1) / K;
+    for (int64_t ch = n_chunks - 1; ch >= 0; --ch) {
+        const int64_t t0 = ch * K;
+        const int kn = int(T - t0 < K ? T - t0 : K);
+        float v[V];
+        bool y[V];
+        if (ch == 0) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                v[j] = c.rest;
+                y[j] = false;
+            }
+        } else {
+            load_f32<V>(saved + (ch - 1) * N + n0, v);
+#pragma unroll
+            for (int j = 0; j < V; ++j) y[j] = v[j] >= c.th;
+        }
+        if (kn == K)
+            backward_chunk<IO, RESET, V, K, true>(c, N, t0, kn, n0, x, gs, gx, v, y, g);
+        else
+            backward_chunk<IO, RESET, V, K, false>(c, N, t0, kn, n0, x, gs, gx, v, y, g);
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Per-feature gain between stacked layers.  grid.x covers the N neurons of a row, V per
+// lane; grid.y strides over rows.
+template <int SPK, int V>
+__device__ __forceinline__ void load_spikes(const uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0,
+                                            float (&y)[V]) {
+    if constexpr (SPK == SNN_SPK_U8) {
+        if constexpr (V == 4) {
+            const uint32_t w = *reinterpret_cast<const uint32_t*>(s + t * row_bytes + n0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) y[j] = float((w >> (8 * j)) & 0xffu);
+        } else {
+            y[0] = float(s[t * row_bytes + n0]);
+        }
+    } else {
+        const uint32_t b = s[t * row_bytes + (n0 >> 3)];
+#pragma unroll
+        for (int j = 0; j < V; ++j) y[j] = float((b >> ((n0 + j) & 7)) & 1u);
+    }
+}
+
+template <int IO, int SPK, int V>
+__global__ __launch_bounds__(kBlock) void gain_forward_kernel(int64_t T, int64_t N, int64_t F,
+                                                              const uint8_t* __restrict__ spikes,
+                                                              int64_t row_bytes,
+                                                              const float* __restrict__ gain,
+                                                              void* __restrict__ x_next) {
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    if (n0 >= N) return;
+    float gv[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
+    for (int64_t t = blockIdx.y; t < T; t += gridDim.y) {
+        float y[V], out[V];
+        load_spikes<SPK, V>(spikes, row_bytes, t, n0, y);
+#pragma unroll
+        for (int j = 0; j < V; ++j) out[j] = gv[j] * y[j];
+        IoVec<IO, V>::store(x_next, t * N + n0, out);
+    }
+}
+
+template <int IO, int V>
+__global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_t N, int64_t F,
+                                                               const void* gx_next,
+                                                               const float* __restrict__ gain,
+                                                               void* gs) {
+    using Io = IoVec<IO, V>;
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    if (n0 >= N) return;
+    float gv[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
+    for (int64_t t = blockIdx.y; t < T; t += gridDim.y) {
+        const typename Io::raw r = Io::load(gx_next, t * N + n0);
+        float out[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) out[j] = gv[j] * Io::get(r, j);
+        Io::store(gs, t * N + n0, out);
+    }
+}
+
+// ------------------------------------------------------------------------------------
+// Host side.
+
+template <typename Tuple, size_t... I>
+void fill_argv(Tuple& t, void** argv, std::index_sequence<I...>) {
+    ((argv[I] = static_cast<void*>(&std::get<I>(t))), ...);
+}
+
+// Launch through hipLaunchKernel so the runtime's verdict is returned directly and the
+// caller's sticky error state is left alone.
+template <typename... P, typename... A>
+snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
+    static_assert(sizeof...(P) == sizeof...(A), "argument count");
+    std::tuple<P...> args(a...);
+    void* argv[sizeof...(P)];
+    fill_argv(args, argv, std::index_sequence_for<P...>{});
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(kBlock), argv, 0, stream);
+    return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
+}
+
+snn_status check_cfg(const snn_lif_cfg* c) {
+    if (c == nullptr) return SNN_E_NULL;
+    if (!(c->decay >= 0.0f && c->decay <= 1.0f)) return SNN_E_PARAM;  // also rejects NaN
+    if (!std::isfinite(c->v_th) || !std::isfinite(c->v_reset)) return SNN_E_PARAM;
+    if (!(c->alpha > 0.0f) || !std::isfinite(c->alpha)) return SNN_E_PARAM;
+    if (c->reset != SNN_RESET_HARD && c->reset != SNN_RESET_SOFT) return SNN_E_PARAM;
+    if (c->io != SNN_IO_F32 && c->io != SNN_IO_BF16) return SNN_E_PARAM;
+    if (c->spk != SNN_SPK_U8 && c->spk != SNN_SPK_BITS) return SNN_E_PARAM;
+    return SNN_OK;
+}
+
+snn_status check_shape(int64_t T, int64_t N) {
+    if (T < 0 || N < 0 || T > kMaxT || N > kMaxN) return SNN_E_SHAPE;
+    if (T > 0 && N > kMaxTN / T) return SNN_E_SHAPE;
+    return SNN_OK;
+}
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t spike_row_bytes(const snn_lif_cfg* c, int64_t N) {
+    return c->spk == SNN_SPK_U8 ? N : 8 * ((N + 63) / 64);
+}
+
+// Neurons per lane and steps per chunk.  The same choice drives the forward, the backward
+// and the checkpoint layout, so it depends only on (cfg, N).
+struct Plan {
+    int v;           // neurons per lane: 4 when N % 4 == 0, else 1
+    int k;           // steps per chunk (= checkpoint interval)
+    int64_t lanes;   // lanes in the forward grid
+    int64_t row_bytes;
+};
+
+constexpr int kChunkVec = 16;
+constexpr int kChunkScalar = 32;
+
+Plan make_plan(const snn_lif_cfg* c, int64_t N) {
+    Plan p;
+    p.v = (N % 4 == 0) ? 4 : 1;
+    p.k = p.v == 4 ? kChunkVec : kChunkScalar;
+    p.row_bytes = spike_row_bytes(c, N);
+    const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
+    p.lanes = (covered + p.v - 1) / p.v;
+    return p;
+}
+
+int64_t saved_bytes(const Plan& p, int64_t T, int64_t N) {
+    const int64_t chunks = (T + p.k - 1) / p.k;
+    return chunks > 1 ? (chunks - 1) * N * int64_t(sizeof(float)) : 0;
+}
+
+LifK kernel_consts(const snn_lif_cfg* c) {
+    LifK k;
+    k.k = c->decay;
+    k.th = c->v_th;
+    k.rest = c->v_reset;
+    k.alpha = c->alpha;
+    k.c_exp = float(-double(c->alpha) * 1.4426950408889634074);  // -alpha log2(e)
+    k.kth = c->decay * c->v_th;
+    return k;
+}
+
+dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
+
+template <int IO, int SPK, int RESET>
+snn_status forward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, void* spikes,
+                          void* saved, float* v_out, hipStream_t s) {
+    uint8_t* sp = static_cast<uint8_t*>(spikes);
+    float* sv = static_cast<float*>(saved);
+    if (p.v == 4)
+        return launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec>, grid_for(p.lanes), s, k, T, N, x, sp,
+                      p.row_bytes, sv, v_out);
+    return launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar>, grid_for(p.lanes), s, k, T, N, x, sp,
+                  p.row_bytes, sv, v_out);
+}
+
+template <int IO, int RESET>
+snn_status backward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
+                           const void* saved, const void* gs, void* gx, hipStream_t s) {
+    const float* sv = static_cast<const float*>(saved);
+    const int64_t lanes = (N + p.v - 1) / p.v;
+    if (p.v == 4)
+        return launch(lif_backward_kernel<IO, RESET, 4, kChunkVec>, grid_for(lanes), s, k, T, N, x, sv, gs, gx);
+    return launch(lif_backward_kernel<IO, RESET, 1, kChunkScalar>, grid_for(lanes), s, k, T, N, x, sv, gs, gx);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* snn_status_str(snn_status status) {
+    switch (status) {
+        case SNN_OK: return "ok";
+        case SNN_E_NULL: return "a required pointer is NULL";
+        case SNN_E_SHAPE: return "shape out of range";
+        case SNN_E_PARAM: return "hyper-parameter or enum out of range";
+        case SNN_E_ALIGN: return "data pointer not 16-byte aligned";
+        case SNN_E_UNSUPPORTED: return "unsupported combination";
+        case SNN_E_LAUNCH: return "kernel launch rejected by the HIP runtime";
+    }
+    return "unknown status";
+}
+
+snn_status snn_spike_row_bytes(const snn_lif_cfg* cfg, int64_t N, size_t* bytes) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if (bytes == nullptr) return SNN_E_NULL;
+    if ((st = check_shape(0, N)) != SNN_OK) return st;
+    *bytes = size_t(spike_row_bytes(cfg, N));
+    return SNN_OK;
+}
+
+snn_status snn_lif_saved_bytes(const snn_lif_cfg* cfg, int64_t T, int64_t N, size_t* bytes) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if (bytes == nullptr) return SNN_E_NULL;
+    if ((st = check_shape(T, N)) != SNN_OK) return st;
+    *bytes = (T == 0 || N == 0) ? 0 : size_t(saved_bytes(make_plan(cfg, N), T, N));
+    return SNN_OK;
+}
+
+snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, void* spikes,
+                           void* saved, float* v_out, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_shape(T, N)) != SNN_OK) return st;
+    if (T == 0 || N == 0) return SNN_OK;
+    const Plan p = make_plan(cfg, N);
+    const bool need_saved = saved_bytes(p, T, N) > 0;
+    if (x == nullptr || spikes == nullptr || (need_saved && saved == nullptr)) return SNN_E_NULL;
+    if (!aligned(x) || !aligned(spikes) || (saved && !aligned(saved)) || (v_out && !aligned(v_out)))
+        return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool bits = cfg->spk == SNN_SPK_BITS, soft = cfg->reset == SNN_RESET_SOFT;
+    if (cfg->io == SNN_IO_F32) {
+        if (bits)
+            return soft ? forward_launch<SNN_IO_F32, SNN_SPK_BITS, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
+                        : forward_launch<SNN_IO_F32, SNN_SPK_BITS, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
+        return soft ? forward_launch<SNN_IO_F32, SNN_SPK_U8, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
+                    : forward_launch<SNN_IO_F32, SNN_SPK_U8, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
+    }
+    if (bits)
+        return soft ? forward_launch<SNN_IO_BF16, SNN_SPK_BITS, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
+                    : forward_launch<SNN_IO_BF16, SNN_SPK_BITS, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
+    return soft ? forward_launch<SNN_IO_BF16, SNN_SPK_U8, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
+                : forward_launch<SNN_IO_BF16, SNN_SPK_U8, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
+}
+
+snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const void* saved,
+                            const void* grad_s, void* grad_x, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_shape(T, N)) != SNN_OK) return st;
+    if (T == 0 || N == 0) return SNN_OK;
+    const Plan p = make_plan(cfg, N);
+    const bool need_saved = saved_bytes(p, T, N) > 0;
+    if (x == nullptr || grad_s == nullptr || grad_x == nullptr || (need_saved && saved == nullptr))
+        return SNN_E_NULL;
+    if (!aligned(x) || !aligned(grad_s) || !aligned(grad_x) || (saved && !aligned(saved))) return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool soft = cfg->reset == SNN_RESET_SOFT;
+    if (cfg->io == SNN_IO_F32)
+        return soft ? backward_launch<SNN_IO_F32, SNN_RESET_SOFT>(p, k, T, N, x, saved, grad_s, grad_x, s)
+                    : backward_launch<SNN_IO_F32, SNN_RESET_HARD>(p, k, T, N, x, saved, grad_s, grad_x, s);
+    return soft ? backward_launch<SNN_IO_BF16, SNN_RESET_SOFT>(p, k, T, N, x, saved, grad_s, grad_x, s)
+                : backward_launch<SNN_IO_BF16, SNN_RESET_HARD>(p, k, T, N, x, saved, grad_s, grad_x, s);
+}
+
+static snn_status check_gain_shape(int64_t T, int64_t B, int64_t F) {
+    if (T < 0 || B < 0 || F < 0) return SNN_E_SHAPE;
+    if (B > 0 && F > kMaxN / B) return SNN_E_SHAPE;
+    return check_shape(T, B * F);
+}
+
+static dim3 gain_grid(int64_t T, int64_t lanes) {
+    return dim3(unsigned((lanes + kBlock - 1) / kBlock), unsigned(T < 65535 ? T : 65535));
+}
+
+snn_status snn_gain_spikes_forward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes,
+                                   const float* gain, void* x_next, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    if (spikes == nullptr || gain == nullptr || x_next == nullptr) return SNN_E_NULL;
+    if (!aligned(spikes) || !aligned(gain) || !aligned(x_next)) return SNN_E_ALIGN;
+    const int64_t row = spike_row_bytes(cfg, N);
+    const uint8_t* sp = static_cast<const uint8_t*>(spikes);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool v4 = N % 4 == 0;
+    const dim3 grid = gain_grid(T, v4 ? N / 4 : N);
+    const bool bits = cfg->spk == SNN_SPK_BITS;
+    if (cfg->io == SNN_IO_F32) {
+        if (v4)
+            return bits ? launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_BITS, 4>, grid, s, T, N, F, sp, row, gain, x_next)
+                        : launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_U8, 4>, grid, s, T, N, F, sp, row, gain, x_next);
+        return bits ? launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_BITS, 1>, grid, s, T, N, F, sp, row, gain, x_next)
+                    : launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_U8, 1>, grid, s, T, N, F, sp, row, gain, x_next);
+    }
+    if (v4)
+        return bits ? launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_BITS, 4>, grid, s, T, N, F, sp, row, gain, x_next)
+                    : launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_U8, 4>, grid, s, T, N, F, sp, row, gain, x_next);
+    return bits ? launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_BITS, 1>, grid, s, T, N, F, sp, row, gain, x_next)
+                : launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_U8, 1>, grid, s, T, N, F, sp, row, gain, x_next);
+}
+
+snn_status snn_gain_grad_backward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* grad_x_next,
+                                  const float* gain, void* grad_s, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    if (grad_x_next == nullptr || gain == nullptr || grad_s == nullptr) return SNN_E_NULL;
+    if (!aligned(grad_x_next) || !aligned(gain) || !aligned(grad_s)) return SNN_E_ALIGN;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool v4 = N % 4 == 0;
+    const dim3 grid = gain_grid(T, v4 ? N / 4 : N);
+    if (cfg->io == SNN_IO_F32)
+        return v4 ? launch(gain_backward_kernel<SNN_IO_F32, 4>, grid, s, T, N, F, grad_x_next, gain, grad_s)
+                  : launch(gain_backward_kernel<SNN_IO_F32, 1>, grid, s, T, N, F, grad_x_next, gain, grad_s);
+    return v4 ? launch(gain_backward_kernel<SNN_IO_BF16, 4>, grid, s, T, N, F, grad_x_next, gain, grad_s)
+              : launch(gain_backward_kernel<SNN_IO_BF16, 1>, grid, s, T, N, F, grad_x_next, gain, grad_s);
+}
+
+}  // extern "C"

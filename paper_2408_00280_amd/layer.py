@@ -1,0 +1,68 @@
+"""Torch-tensor conveniences over the C ABI: allocate outputs with torch, call the kernels.
+
+Torch provides device memory and streams only; the LIF arithmetic runs in the HIP
+kernels reached through :mod:`paper_2408_00280_amd.native`.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import native
+
+IO_DTYPES = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+@dataclass(frozen=True)
+class LifConfig:
+    """Hyper-parameters of one LIF layer (see snn_lif_cfg in include/snn_lif.h)."""
+    decay: float
+    v_th: float
+    v_reset: float = 0.0
+    alpha: float = 4.0
+    reset: str = "hard"   # "hard" (Eq. (1)) or "soft"
+    io: str = "f32"       # dtype of x, dL/dy, dL/dx
+    spk: str = "u8"       # "u8" or "bits"
+
+    def c(self) -> native.snn_lif_cfg:
+        return native.make_cfg(self.decay, self.v_th, self.v_reset, self.alpha, self.reset, self.io, self.spk)
+
+    @property
+    def dtype(self) -> torch.dtype:
+        return IO_DTYPES[self.io]
+
+
+def _TN(x: torch.Tensor):
+    T = x.shape[0]
+    return T, (x.numel() // T if T else 0)
+
+
+def alloc_forward(cfg: LifConfig, T: int, N: int, device, v_out: bool = False):
+    """(spikes [T][row_bytes] uint8, saved uint8 bytes, v [T][N] float32 or None)."""
+    c = cfg.c()
+    row = native.snn_spike_row_bytes(c, N)
+    spikes = torch.empty((T, row), dtype=torch.uint8, device=device)
+    saved = torch.empty(native.snn_lif_saved_bytes(c, T, N), dtype=torch.uint8, device=device)
+    v = torch.empty((T, N), dtype=torch.float32, device=device) if v_out else None
+    return spikes, saved, v
+
+
+def forward(cfg: LifConfig, x: torch.Tensor, *, v_out: bool = False, out=None, stream=None):
+    """Fused forward of x[T, ...] (cfg.dtype, contiguous).  Returns (spikes, saved, v_or_None)."""
+    assert x.dtype == cfg.dtype and x.is_contiguous()
+    T, N = _TN(x)
+    spikes, saved, v = out if out is not None else alloc_forward(cfg, T, N, x.device, v_out)
+    native.snn_lif_forward(cfg.c(), T, N, x, spikes, saved if saved.numel() else None, v, stream)
+    return spikes, saved, v
+
+
+def backward(cfg: LifConfig, x: torch.Tensor, saved: torch.Tensor, grad_s: torch.Tensor, *,
+             grad_x: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Fused backward; returns dL/dx with x's shape and dtype (in place if grad_x is grad_s)."""
+    assert grad_s.dtype == cfg.dtype and grad_s.shape == x.shape and grad_s.is_contiguous()
+    T, N = _TN(x)
+    if grad_x is None:
+        grad_x = torch.empty_like(grad_s)
+    native.snn_lif_backward(cfg.c(), T, N, x, saved if saved.numel() else None, grad_s, grad_x, stream)
+    return grad_x
