@@ -48,32 +48,55 @@ struct LifK {
 };
 
 // ------------------------------------------------------------------------------------
+// Streaming memory access.  Every tensor element is touched once per kernel, so loads
+// and stores carry the non-temporal hint.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+template <typename E>
+__device__ __forceinline__ E ld_nt(const void* p) {
+    return __builtin_nontemporal_load(static_cast<const E*>(p));
+}
+
+template <typename E>
+__device__ __forceinline__ void st_nt(void* p, E v) {
+    __builtin_nontemporal_store(v, static_cast<E*>(p));
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup b runs on XCD b % 8).
+// Renumber them so that each XCD walks one contiguous range of the neuron axis: with the
+// 32 MiB-apart rows of a [T][N] walk, this keeps each XCD's concurrent accesses local.
+constexpr unsigned kXcds = 8;
+
+__device__ __forceinline__ int64_t xcd_contiguous_block() {
+    const unsigned nb = gridDim.x, b = blockIdx.x;
+    const unsigned xcd = b % kXcds, slot = b / kXcds, q = nb / kXcds, r = nb % kXcds;
+    return int64_t(xcd) * q + (xcd < r ? xcd : r) + slot;
+}
+
+// ------------------------------------------------------------------------------------
 // Vectors of V consecutive neurons in the I/O dtype.
 template <int IO, int V>
 struct IoVec;
 
 template <>
 struct IoVec<SNN_IO_F32, 4> {
-    using raw = float4;
-    __device__ static raw load(const void* b, int64_t i) {
-        return *reinterpret_cast<const float4*>(static_cast<const float*>(b) + i);
-    }
-    __device__ static float get(const raw& r, int j) {
-        return j == 0 ? r.x : j == 1 ? r.y : j == 2 ? r.z : r.w;
-    }
+    using raw = f32x4_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const float*>(b) + i); }
+    __device__ static float get(const raw& r, int j) { return r[j]; }
     __device__ static void store(void* b, int64_t i, const float (&f)[4]) {
-        *reinterpret_cast<float4*>(static_cast<float*>(b) + i) = make_float4(f[0], f[1], f[2], f[3]);
+        const raw v = {f[0], f[1], f[2], f[3]};
+        st_nt(static_cast<float*>(b) + i, v);
     }
 };
 
 template <>
 struct IoVec<SNN_IO_F32, 1> {
     using raw = float;
-    __device__ static raw load(const void* b, int64_t i) { return static_cast<const float*>(b)[i]; }
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const float*>(b) + i); }
     __device__ static float get(const raw& r, int) { return r; }
-    __device__ static void store(void* b, int64_t i, const float (&f)[1]) {
-        static_cast<float*>(b)[i] = f[0];
-    }
+    __device__ static void store(void* b, int64_t i, const float (&f)[1]) { st_nt(static_cast<float*>(b) + i, f[0]); }
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -85,51 +108,27 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
-template <>
-struct IoVec<SNN_IO_BF16, 8> {
-    using raw = uint4;
-    __device__ static raw load(const void* b, int64_t i) {
-        return *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(b) + i);
-    }
-    __device__ static float get(const raw& r, int j) {
-        const uint32_t w = (j >> 1) == 0 ? r.x : (j >> 1) == 1 ? r.y : (j >> 1) == 2 ? r.z : r.w;
-        return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
-    }
-    __device__ static void store(void* b, int64_t i, const float (&f)[8]) {
-        uint4 w;
-        w.x = pack_bf16x2(f[0], f[1]);
-        w.y = pack_bf16x2(f[2], f[3]);
-        w.z = pack_bf16x2(f[4], f[5]);
-        w.w = pack_bf16x2(f[6], f[7]);
-        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(b) + i) = w;
-    }
-};
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 template <>
 struct IoVec<SNN_IO_BF16, 4> {
-    using raw = uint2;
-    __device__ static raw load(const void* b, int64_t i) {
-        return *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(b) + i);
-    }
-    __device__ static float get(const raw& r, int j) {
-        const uint32_t w = (j >> 1) == 0 ? r.x : r.y;
-        return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
-    }
+    using raw = u32x2_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const uint16_t*>(b) + i); }
+    __device__ static float get(const raw& r, int j) { return (j & 1) ? bf16_hi(r[j >> 1]) : bf16_lo(r[j >> 1]); }
     __device__ static void store(void* b, int64_t i, const float (&f)[4]) {
-        uint2 w;
-        w.x = pack_bf16x2(f[0], f[1]);
-        w.y = pack_bf16x2(f[2], f[3]);
-        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(b) + i) = w;
+        const raw w = {pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3])};
+        st_nt(static_cast<uint16_t*>(b) + i, w);
     }
 };
 
 template <>
 struct IoVec<SNN_IO_BF16, 1> {
-    using raw = uint32_t;
-    __device__ static raw load(const void* b, int64_t i) { return static_cast<const uint16_t*>(b)[i]; }
-    __device__ static float get(const raw& r, int) { return __uint_as_float(r << 16); }
+    using raw = uint16_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const uint16_t*>(b) + i); }
+    __device__ static float get(const raw& r, int) { return __uint_as_float(uint32_t(r) << 16); }
     __device__ static void store(void* b, int64_t i, const float (&f)[1]) {
-        static_cast<uint16_t*>(b)[i] = static_cast<uint16_t>(pack_bf16x2(f[0], 0.0f) & 0xffffu);
+        st_nt(static_cast<uint16_t*>(b) + i, static_cast<uint16_t>(pack_bf16x2(f[0], 0.0f) & 0xffffu));
     }
 };
 
@@ -166,18 +165,7 @@ struct SpikeOut<SNN_SPK_U8, 4> {
                                  const bool (&y)[4]) {
         const uint32_t w = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) |
                            (uint32_t(y[3]) << 24);
-        if (active) *reinterpret_cast<uint32_t*>(s + t * row_bytes + n0) = w;
-    }
-};
-
-template <>
-struct SpikeOut<SNN_SPK_U8, 8> {
-    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
-                                 const bool (&y)[8]) {
-        uint2 w;
-        w.x = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) | (uint32_t(y[3]) << 24);
-        w.y = uint32_t(y[4]) | (uint32_t(y[5]) << 8) | (uint32_t(y[6]) << 16) | (uint32_t(y[7]) << 24);
-        if (active) *reinterpret_cast<uint2*>(s + t * row_bytes + n0) = w;
+        if (active) st_nt(s + t * row_bytes + n0, w);
     }
 };
 
@@ -185,32 +173,21 @@ template <>
 struct SpikeOut<SNN_SPK_U8, 1> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[1]) {
-        if (active) s[t * row_bytes + n0] = uint8_t(y[0]);
+        if (active) st_nt(s + t * row_bytes + n0, uint8_t(y[0]));
     }
 };
 
 // Bits, 4 neurons per lane: lanes 2j and 2j+1 share a byte; the odd lane's nibble is
 // moved to the even lane with a DPP quad permutation [1,0,3,2].  Every lane of the wave
-// must execute this (no divergence around it).
+// executes this (no divergence around it).
 template <>
 struct SpikeOut<SNN_SPK_BITS, 4> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[4]) {
-        int nib = active ? (int(y[0]) | (int(y[1]) << 1) | (int(y[2]) << 2) | (int(y[3]) << 3)) : 0;
+        const int nib = active ? (int(y[0]) | (int(y[1]) << 1) | (int(y[2]) << 2) | (int(y[3]) << 3)) : 0;
         const int other = __builtin_amdgcn_mov_dpp(nib, 0xB1, 0xF, 0xF, false);
         if (((n0 >> 2) & 1) == 0 && n0 < row_bytes * 8)
-            s[t * row_bytes + (n0 >> 3)] = uint8_t(nib | (other << 4));
-    }
-};
-
-template <>
-struct SpikeOut<SNN_SPK_BITS, 8> {
-    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
-                                 const bool (&y)[8]) {
-        uint32_t b = 0;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) b |= uint32_t(y[j]) << j;
-        if (n0 < row_bytes * 8) s[t * row_bytes + (n0 >> 3)] = uint8_t(active ? b : 0u);
+            st_nt(s + t * row_bytes + (n0 >> 3), uint8_t(nib | (other << 4)));
     }
 };
 
@@ -221,45 +198,38 @@ struct SpikeOut<SNN_SPK_BITS, 1> {
                                  const bool (&y)[1]) {
         const uint64_t word = __ballot(active && y[0]);
         if ((threadIdx.x & (kWave - 1)) == 0 && n0 < row_bytes * 8)
-            *reinterpret_cast<uint64_t*>(s + t * row_bytes + (n0 >> 3)) = word;
+            st_nt(s + t * row_bytes + (n0 >> 3), word);
     }
 };
-
 
 // ------------------------------------------------------------------------------------
 // fp32 rows of V neurons (checkpoints and the optional membrane output).
 template <int V>
 __device__ __forceinline__ void store_f32(float* p, const float (&f)[V]) {
-    if constexpr (V % 4 == 0) {
-#pragma unroll
-        for (int q = 0; q < V / 4; ++q)
-            reinterpret_cast<float4*>(p)[q] = make_float4(f[4 * q], f[4 * q + 1], f[4 * q + 2], f[4 * q + 3]);
+    if constexpr (V == 4) {
+        const f32x4_t v = {f[0], f[1], f[2], f[3]};
+        st_nt(p, v);
     } else {
-#pragma unroll
-        for (int j = 0; j < V; ++j) p[j] = f[j];
+        st_nt(p, f[0]);
     }
 }
 
 template <int V>
 __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
-    if constexpr (V % 4 == 0) {
-#pragma unroll
-        for (int q = 0; q < V / 4; ++q) {
-            const float4 a = reinterpret_cast<const float4*>(p)[q];
-            f[4 * q] = a.x;
-            f[4 * q + 1] = a.y;
-            f[4 * q + 2] = a.z;
-            f[4 * q + 3] = a.w;
-        }
+    if constexpr (V == 4) {
+        const f32x4_t a = ld_nt<f32x4_t>(p);
+        f[0] = a[0];
+        f[1] = a[1];
+        f[2] = a[2];
+        f[3] = a[3];
     } else {
-#pragma unroll
-        for (int j = 0; j < V; ++j) f[j] = p[j];
+        f[0] = ld_nt<float>(p);
     }
 }
 
 // ------------------------------------------------------------------------------------
 // Forward: one chunk of up to K steps.  FULL chunks skip the per-step bound test.
-template <int IO, int SPK, int RESET, int V, int K, bool FULL>
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL>
 __device__ __forceinline__ void forward_chunk(const LifK& c, int64_t N, int64_t t0, int kn, int64_t n0,
                                               bool active, const void* __restrict__ x,
                                               uint8_t* __restrict__ spikes, int64_t row_bytes,
@@ -277,21 +247,21 @@ __device__ __forceinline__ void forward_chunk(const LifK& c, int64_t N, int64_t 
 #pragma unroll
             for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], active ? Io::get(xr[i], j) : 0.0f);
             SpikeOut<SPK, V>::store(spikes, row_bytes, t0 + i, n0, active, y);
-            if (v_out != nullptr && active) store_f32<V>(v_out + (t0 + i) * N + n0, v);
+            if (VOUT && active) store_f32<V>(v_out + (t0 + i) * N + n0, v);
         }
     }
 }
 
 // Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
 // N load nothing and report no spikes; they exist only to complete spike-bit words.
-template <int IO, int SPK, int RESET, int V, int K>
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT>
 __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
                                                              const void* __restrict__ x,
                                                              uint8_t* __restrict__ spikes,
                                                              int64_t row_bytes,
                                                              float* __restrict__ saved,
                                                              float* __restrict__ v_out) {
-    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     const bool active = n0 < N;
     float v[V];
     bool y[V];
@@ -305,9 +275,9 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
         const int64_t t0 = ch * K;
         const int kn = int(T - t0 < K ? T - t0 : K);
         if (kn == K)
-            forward_chunk<IO, SPK, RESET, V, K, true>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
+            forward_chunk<IO, SPK, RESET, V, K, VOUT, true>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
         else
-            forward_chunk<IO, SPK, RESET, V, K, false>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
+            forward_chunk<IO, SPK, RESET, V, K, VOUT, false>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
         if (ch + 1 < n_chunks && active) store_f32<V>(saved + ch * N + n0, v);
     }
 }
@@ -370,7 +340,7 @@ __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T,
                                                               const void* __restrict__ x,
                                                               const float* __restrict__ saved,
                                                               const void* gs, void* gx) {
-    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     if (n0 >= N) return;
     float g[V];
 #pragma unroll
@@ -400,21 +370,20 @@ __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T,
 }
 
 // ------------------------------------------------------------------------------------
-// Per-feature gain between stacked layers.  grid.x covers the N neurons of a row, V per
-// lane; grid.y strides over rows.
+// Per-feature gain between stacked layers.  One lane per V neurons walks all T rows.
 template <int SPK, int V>
 __device__ __forceinline__ void load_spikes(const uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0,
                                             float (&y)[V]) {
     if constexpr (SPK == SNN_SPK_U8) {
         if constexpr (V == 4) {
-            const uint32_t w = *reinterpret_cast<const uint32_t*>(s + t * row_bytes + n0);
+            const uint32_t w = ld_nt<uint32_t>(s + t * row_bytes + n0);
 #pragma unroll
             for (int j = 0; j < 4; ++j) y[j] = float((w >> (8 * j)) & 0xffu);
         } else {
-            y[0] = float(s[t * row_bytes + n0]);
+            y[0] = float(ld_nt<uint8_t>(s + t * row_bytes + n0));
         }
     } else {
-        const uint32_t b = s[t * row_bytes + (n0 >> 3)];
+        const uint32_t b = ld_nt<uint8_t>(s + t * row_bytes + (n0 >> 3));
 #pragma unroll
         for (int j = 0; j < V; ++j) y[j] = float((b >> ((n0 + j) & 7)) & 1u);
     }
@@ -426,12 +395,12 @@ __global__ __launch_bounds__(kBlock) void gain_forward_kernel(int64_t T, int64_t
                                                               int64_t row_bytes,
                                                               const float* __restrict__ gain,
                                                               void* __restrict__ x_next) {
-    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     if (n0 >= N) return;
     float gv[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
-    for (int64_t t = blockIdx.y; t < T; t += gridDim.y) {
+    for (int64_t t = 0; t < T; ++t) {
         float y[V], out[V];
         load_spikes<SPK, V>(spikes, row_bytes, t, n0, y);
 #pragma unroll
@@ -446,12 +415,12 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
                                                                const float* __restrict__ gain,
                                                                void* gs) {
     using Io = IoVec<IO, V>;
-    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     if (n0 >= N) return;
     float gv[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
-    for (int64_t t = blockIdx.y; t < T; t += gridDim.y) {
+    for (int64_t t = 0; t < T; ++t) {
         const typename Io::raw r = Io::load(gx_next, t * N + n0);
         float out[V];
 #pragma unroll
@@ -548,11 +517,12 @@ snn_status forward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, co
                           void* saved, float* v_out, hipStream_t s) {
     uint8_t* sp = static_cast<uint8_t*>(spikes);
     float* sv = static_cast<float*>(saved);
+    const dim3 g = grid_for(p.lanes);
     if (p.v == 4)
-        return launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec>, grid_for(p.lanes), s, k, T, N, x, sp,
-                      p.row_bytes, sv, v_out);
-    return launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar>, grid_for(p.lanes), s, k, T, N, x, sp,
-                  p.row_bytes, sv, v_out);
+        return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec, true>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
+                     : launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec, false>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
+    return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar, true>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
+                 : launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar, false>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
 }
 
 template <int IO, int RESET>
@@ -655,9 +625,7 @@ static snn_status check_gain_shape(int64_t T, int64_t B, int64_t F) {
     return check_shape(T, B * F);
 }
 
-static dim3 gain_grid(int64_t T, int64_t lanes) {
-    return dim3(unsigned((lanes + kBlock - 1) / kBlock), unsigned(T < 65535 ? T : 65535));
-}
+static dim3 gain_grid(int64_t lanes) { return grid_for(lanes); }
 
 snn_status snn_gain_spikes_forward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes,
                                    const float* gain, void* x_next, void* stream) {
@@ -672,7 +640,7 @@ snn_status snn_gain_spikes_forward(const snn_lif_cfg* cfg, int64_t T, int64_t B,
     const uint8_t* sp = static_cast<const uint8_t*>(spikes);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool v4 = N % 4 == 0;
-    const dim3 grid = gain_grid(T, v4 ? N / 4 : N);
+    const dim3 grid = gain_grid(v4 ? N / 4 : N);
     const bool bits = cfg->spk == SNN_SPK_BITS;
     if (cfg->io == SNN_IO_F32) {
         if (v4)
@@ -699,7 +667,7 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg* cfg, int64_t T, int64_t B, 
     if (!aligned(grad_x_next) || !aligned(gain) || !aligned(grad_s)) return SNN_E_ALIGN;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool v4 = N % 4 == 0;
-    const dim3 grid = gain_grid(T, v4 ? N / 4 : N);
+    const dim3 grid = gain_grid(v4 ? N / 4 : N);
     if (cfg->io == SNN_IO_F32)
         return v4 ? launch(gain_backward_kernel<SNN_IO_F32, 4>, grid, s, T, N, F, grad_x_next, gain, grad_s)
                   : launch(gain_backward_kernel<SNN_IO_F32, 1>, grid, s, T, N, F, grad_x_next, gain, grad_s);
