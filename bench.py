@@ -1,15 +1,19 @@
 #!/usr/bin/env python3
 """Benchmark of the temporally fused LIF layer on one MI355X.
 
-One step = the fused forward plus the fused backward of the conv-shaped LIF layer
+Default step = the fused forward plus the fused backward of the conv-shaped LIF layer
 x[T=16, B=64, C=128, H=32, W=32] (fp32 I/O, u8 spikes, decay 0.5, V_th 1, hard reset,
 sigmoid surrogate alpha = 4), with seeded synthetic inputs already resident in HBM.
 Prints ONE JSON line: neuron-timesteps/s over the timed steps, the HBM roofline of the
-dominant kernel (the backward) from HIP events recorded on the launch stream, and the CPU
-oracle's throughput on the host as a baseline.
+dominant kernel (the backward) from HIP events recorded on the launch stream around every
+launch, and the CPU oracle's throughput on the host as a baseline.
 
     python bench.py [--steps K] [--warmup W] [--workload conv|single|long|stack|large]
                     [--T T] [--no-cpu-baseline] [--with-copy]
+
+Workloads whose buffers are smaller than the 256 MB Infinity Cache rotate over several
+independent buffer sets (about 1 GiB in total), one set per step, so that a step does not
+find the previous step's data in the cache.
 """
 from __future__ import annotations
 
@@ -27,14 +31,16 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
 KERNEL_SRC = os.path.join(ROOT, "paper_2408_00280_amd", "csrc", "snn_lif.hip")
 PROFILES = os.path.join(ROOT, "profiles")
+ROTATE_BYTES = 1 << 30
 
 
-def bytes_per_nts(w, layers: int = 1):
+def bytes_per_nts(w):
     """Algorithmic HBM bytes per neuron-timestep: each I/O tensor read or written once.
-    forward: read x, write spikes; backward: read x (recompute) and dL/dy, write dL/dx."""
+    LIF forward: read x, write spikes; LIF backward: read x (recompute) and dL/dy, write
+    dL/dx; gain forward: read spikes, write x_next; gain backward: read and write."""
     e = 4 if w.io == "f32" else 2
     s = 1.0 if w.spk == "u8" else 0.125
-    return {"forward": e + s, "backward": 3 * e}
+    return {"lif_forward": e + s, "lif_backward": 3 * e, "gain_forward": s + e, "gain_backward": 2 * e}
 
 
 def source_hash() -> str:
@@ -56,18 +62,26 @@ def measured_traffic(kernel_tag: str, workload_tag: str):
     return float(m_val.group(1))
 
 
-def cpu_baseline(w, x_np, gs_np):
-    """The CPU oracle, single-threaded, on the same inputs (forward + backward)."""
+def cpu_baseline(w, x_np, gs_np, gains=None):
+    """The CPU oracle, single-threaded, forward + backward on the given inputs."""
     import oracle
     p = oracle.Params.of(w.params)
     t0 = time.perf_counter()
-    y, v = oracle.forward(p, x_np)
-    oracle.backward(p, v, y, gs_np)
+    if gains is None:
+        y, v = oracle.forward(p, x_np)
+        oracle.backward(p, v, y, gs_np)
+        layers = 1
+    else:
+        B = x_np.shape[1] // w.F
+        _, ys, vs = oracle.stack_forward(p, x_np, gains, B, w.F)
+        oracle.stack_backward(p, ys, vs, gs_np, gains, B, w.F)
+        layers = len(gains) + 1
     dt = time.perf_counter() - t0
-    nts = x_np.shape[0] * x_np.shape[1]
+    nts = layers * x_np.shape[0] * x_np.shape[1]
     return {"value": nts / dt, "unit": "neuron-timesteps/s", "cores": 1, "kind": "oracle",
-            "sample": f"whole workload: {x_np.shape[0]} steps x {x_np.shape[1]} neurons "
-                      f"({nts} nts), forward + backward, {dt:.2f} s"}
+            "sample": f"{layers} layer(s) x {x_np.shape[0]} steps x {x_np.shape[1]} neurons "
+                      f"({nts} nts, {'the whole workload' if x_np.shape[1] == w.N else 'the first neurons'}), "
+                      f"forward + backward, {dt:.2f} s"}
 
 
 def main():
@@ -90,28 +104,29 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2408_00280_amd import layer
+    import synth
+    from paper_2408_00280_amd import layer, native
     from synth import workloads as W
 
     w = W.WORKLOADS[args.workload]
     if args.T:
         w = w.with_T(args.T)
-    if w.layers != 1:
-        sys.exit("bench.py times single-layer workloads; the stack is covered by the tests")
     dev = torch.device("cuda:0")
     cfg = layer.LifConfig(w.params.decay, w.params.v_th, w.params.v_reset, w.params.alpha,
                           w.params.reset, w.io, w.spk)
-    T, N = w.T, w.N
+    c = cfg.c()
+    T, N, L = w.T, w.N, w.layers
     dt = layer.IO_DTYPES[w.io]
+    esz = 4 if w.io == "f32" else 2
+    B, F = (N // w.F, w.F)
 
     # seeded inputs, generated on the host in row chunks and copied to HBM
     keep_host = not args.no_cpu_baseline and T * N <= (1 << 28)
-    x = torch.empty((T, N), dtype=dt, device=dev)
-    gs = torch.empty((T, N), dtype=dt, device=dev)
+    x0 = torch.empty((T, N), dtype=dt, device=dev)
+    gs0 = torch.empty((T, N), dtype=dt, device=dev)
     host = {"x": [], "gs": []}
     rows = max(1, (1 << 26) // N)
-    import synth
-    for name, gen, dst in (("x", W.x_rows, x), ("gs", W.gs_rows, gs)):
+    for name, gen, dst in (("x", W.x_rows, x0), ("gs", W.gs_rows, gs0)):
         for t0 in range(0, T, rows):
             a = gen(w, t0, min(T, t0 + rows))
             if keep_host:
@@ -121,36 +136,82 @@ def main():
             else:
                 bits = synth.to_bf16_bits(a).view(np.int16)
                 dst[t0:t0 + a.shape[0]].copy_(torch.from_numpy(bits).view(torch.bfloat16))
-    spikes, saved, _ = layer.alloc_forward(cfg, T, N, dev)
-    gx = torch.empty_like(gs)
+    gains_np = [W.gain(w, l) for l in range(L - 1)]
+    gains = [torch.from_numpy(g).to(dev) for g in gains_np]
+
+    # buffer sets: x / spikes / checkpoints per layer, one dL/dy-dL/dx pair per layer
+    row = native.snn_spike_row_bytes(c, N)
+    sbytes = native.snn_lif_saved_bytes(c, T, N)
+    set_bytes = L * T * (2 * N * esz + row) + 2 * T * N * esz + L * sbytes
+    R = max(1, min(64, -(-ROTATE_BYTES // set_bytes))) if set_bytes < (512 << 20) else 1
+    sets = []
+    for _ in range(R):
+        st = {"x": [x0.clone() if R > 1 else x0] + [torch.empty_like(x0) for _ in range(L - 1)],
+              "spk": [torch.empty((T, row), dtype=torch.uint8, device=dev) for _ in range(L)],
+              "saved": [torch.empty(sbytes, dtype=torch.uint8, device=dev) if sbytes else None for _ in range(L)],
+              "gs": gs0.clone() if R > 1 else gs0,
+              "g": [torch.empty_like(gs0) for _ in range(L)]}
+        sets.append(st)
     stream = torch.cuda.current_stream()
+    s_ptr = stream.cuda_stream
     torch.cuda.synchronize()
 
-    def step(ev=None, i=0):
-        if ev is not None:
-            ev[3 * i].record(stream)
-        layer.forward(cfg, x, out=(spikes, saved, None), stream=stream)
-        if ev is not None:
-            ev[3 * i + 1].record(stream)
-        layer.backward(cfg, x, saved, gs, grad_x=gx, stream=stream)
-        if ev is not None:
-            ev[3 * i + 2].record(stream)
+    bpn = bytes_per_nts(w)
+    nts = T * N
 
-    for _ in range(args.warmup):
-        step()
+    def launches(st):
+        """The kernels of one step, in order: (kernel, algorithmic bytes, call)."""
+        out = []
+        for l in range(L):
+            out.append(("lif_forward", bpn["lif_forward"] * nts, lambda l=l: native.snn_lif_forward(
+                c, T, N, st["x"][l], st["spk"][l], st["saved"][l], None, s_ptr)))
+            if l + 1 < L:
+                out.append(("gain_forward", bpn["gain_forward"] * nts, lambda l=l: native.snn_gain_spikes_forward(
+                    c, T, B, F, st["spk"][l], gains[l], st["x"][l + 1], s_ptr)))
+        for l in range(L - 1, -1, -1):
+            gy = st["gs"] if l == L - 1 else st["g"][l + 1]   # gain backward writes in place
+            out.append(("lif_backward", bpn["lif_backward"] * nts, lambda l=l, gy=gy: native.snn_lif_backward(
+                c, T, N, st["x"][l], st["saved"][l], gy, st["g"][l], s_ptr)))
+            if l > 0:
+                out.append(("gain_backward", bpn["gain_backward"] * nts, lambda l=l: native.snn_gain_grad_backward(
+                    c, T, B, F, st["g"][l], gains[l - 1], st["g"][l], s_ptr)))
+        return out
+
+    plans = [launches(st) for st in sets]
+    n_launch = len(plans[0])
+
+    for i in range(args.warmup):
+        for _, _, f in plans[i % R]:
+            f()
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3 * K)]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range((n_launch + 1) * K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        step(ev, i)
+        base = i * (n_launch + 1)
+        ev[base].record(stream)
+        for j, (_, _, f) in enumerate(plans[i % R]):
+            f()
+            ev[base + j + 1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    fwd_ms = float(np.mean([ev[3 * i].elapsed_time(ev[3 * i + 1]) for i in range(K)]))
-    bwd_ms = float(np.mean([ev[3 * i + 1].elapsed_time(ev[3 * i + 2]) for i in range(K)]))
+    per = {}
+    for i in range(K):
+        base = i * (n_launch + 1)
+        for j, (name, nbytes, _) in enumerate(plans[0]):
+            d = per.setdefault(name, {"ms": [], "bytes": nbytes})
+            d["ms"].append(ev[base + j].elapsed_time(ev[base + j + 1]))
+    kernels = {}
+    for name, d in per.items():
+        ms = float(np.mean(d["ms"]))
+        kernels[name + "_kernel"] = {"avg_launch_ms": ms, "launches_per_step": len(d["ms"]) // K,
+                                     "GB/s": d["bytes"] / (ms * 1e-3) / 1e9,
+                                     "bytes_per_nts": bpn[name]}
+    step_kernel_ms = sum(v["avg_launch_ms"] * v["launches_per_step"] for v in kernels.values())
+    step_bytes = sum(d["bytes"] * len(d["ms"]) / K for d in per.values())
 
     if args.with_copy:   # counter calibration: a plain copy of known size
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
@@ -159,18 +220,13 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
 
-    nts = T * N
-    bpn = bytes_per_nts(w)
-    bwd_bytes = bpn["backward"] * nts
-    fwd_bytes = bpn["forward"] * nts
-    bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
-    fwd_gbs = fwd_bytes / (fwd_ms * 1e-3) / 1e9
     wtag = f"{w.name}_T{T}_N{N}"
-    traffic = measured_traffic("lif_backward", wtag)
-
+    dom = kernels["lif_backward_kernel"]
+    for name in kernels:
+        kernels[name]["traffic"] = measured_traffic(name.replace("_kernel", ""), wtag)
     out = {
         "metric": "neuron-timesteps/sec (LIF fwd+bwd) and % of MI355X HBM peak",
-        "value": nts * K / elapsed,
+        "value": L * nts * K / elapsed,
         "unit": "neuron-timesteps/s",
         "n_gpus": 1,
         "steps": K,
@@ -181,28 +237,25 @@ def main():
         "vs_baseline": None,
         "dtype": "f32" if w.io == "f32" else "bf16 I/O, f32 compute",
         "data": "synthetic (seeded counter-based generator)",
-        "config": {"workload": w.description, "T": T, "N": N, "dims": list(w.dims), "io": w.io,
+        "config": {"workload": w.description, "T": T, "N": N, "layers": L, "dims": list(w.dims), "io": w.io,
                    "spikes": w.spk, "reset": w.params.reset, "decay": w.params.decay,
-                   "v_th": w.params.v_th, "alpha": w.params.alpha, "parallelism": "none (1 GPU)"},
-        "hbm_fraction_fwd_bwd": (fwd_bytes + bwd_bytes) / ((fwd_ms + bwd_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": "lif_backward_kernel", "bound": "hbm", "achieved": bwd_gbs,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": bwd_gbs / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes_per_launch": bwd_bytes,
-                     "bytes_per_nts": bpn["backward"], "avg_launch_ms": bwd_ms},
-        "kernels": {"lif_forward_kernel": {"avg_launch_ms": fwd_ms, "GB/s": fwd_gbs,
-                                           "bytes_per_nts": bpn["forward"],
-                                           "traffic": measured_traffic("lif_forward", wtag)},
-                    "lif_backward_kernel": {"avg_launch_ms": bwd_ms, "GB/s": bwd_gbs,
-                                            "bytes_per_nts": bpn["backward"]}},
+                   "v_th": w.params.v_th, "alpha": w.params.alpha, "buffer_sets": R,
+                   "parallelism": "none (1 GPU)"},
+        "hbm_fraction_step": step_bytes / (step_kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"kernel": "lif_backward_kernel", "bound": "hbm", "achieved": dom["GB/s"],
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom["GB/s"] / HBM_PEAK_GBS,
+                     "traffic": dom["traffic"], "algorithmic_bytes_per_launch": bpn["lif_backward"] * nts,
+                     "bytes_per_nts": bpn["lif_backward"], "avg_launch_ms": dom["avg_launch_ms"]},
+        "kernels": kernels,
         "kernel_source_sha256_16": source_hash(),
     }
     if not args.no_cpu_baseline:
         if keep_host:
             x_np, gs_np = np.concatenate(host["x"]), np.concatenate(host["gs"])
-        else:   # a bounded sample: the first 2^20 neurons over all steps
-            cols = np.arange(min(N, 1 << 20))
+        else:   # a bounded sample: the first neurons over all steps
+            cols = np.arange(min(N, max(1 << 12, (1 << 28) // T)))
             x_np, gs_np = W.x_cols(w, cols), W.gs_cols(w, cols)
-        out["cpu_baseline"] = cpu_baseline(w, x_np, gs_np)
+        out["cpu_baseline"] = cpu_baseline(w, x_np, gs_np, gains_np if L > 1 else None)
     print(json.dumps(out), flush=True)
 
 

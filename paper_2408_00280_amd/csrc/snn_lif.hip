@@ -51,6 +51,7 @@ struct LifK {
 // Streaming memory access.  Every tensor element is touched once per kernel, so loads
 // and stores carry the non-temporal hint.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -92,6 +93,17 @@ struct IoVec<SNN_IO_F32, 4> {
 };
 
 template <>
+struct IoVec<SNN_IO_F32, 2> {
+    using raw = f32x2_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const float*>(b) + i); }
+    __device__ static float get(const raw& r, int j) { return r[j]; }
+    __device__ static void store(void* b, int64_t i, const float (&f)[2]) {
+        const raw v = {f[0], f[1]};
+        st_nt(static_cast<float*>(b) + i, v);
+    }
+};
+
+template <>
 struct IoVec<SNN_IO_F32, 1> {
     using raw = float;
     __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const float*>(b) + i); }
@@ -100,7 +112,6 @@ struct IoVec<SNN_IO_F32, 1> {
 };
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
 // Two floats -> two bf16 (round to nearest even) packed low/high in one dword.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -119,6 +130,16 @@ struct IoVec<SNN_IO_BF16, 4> {
     __device__ static void store(void* b, int64_t i, const float (&f)[4]) {
         const raw w = {pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3])};
         st_nt(static_cast<uint16_t*>(b) + i, w);
+    }
+};
+
+template <>
+struct IoVec<SNN_IO_BF16, 2> {
+    using raw = uint32_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const uint16_t*>(b) + i); }
+    __device__ static float get(const raw& r, int j) { return j ? bf16_hi(r) : bf16_lo(r); }
+    __device__ static void store(void* b, int64_t i, const float (&f)[2]) {
+        st_nt(static_cast<uint16_t*>(b) + i, pack_bf16x2(f[0], f[1]));
     }
 };
 
@@ -155,7 +176,10 @@ __device__ __forceinline__ float surrogate(const LifK& c, float u) {
 }
 
 // ------------------------------------------------------------------------------------
-// Spike rows.  `t` is the row; lanes own neurons [n0, n0 + V).
+// Spike rows.  `t` is the row; lanes own neurons [n0, n0 + V).  A wave's share of a spike
+// row can be less than a cache line (bits, or one byte per lane), so spikes are written
+// with ordinary stores: the L2 merges the partial lines of neighbouring waves before they
+// reach HBM, and a following kernel that reads the spikes can find them in cache.
 template <int SPK, int V>
 struct SpikeOut;
 
@@ -165,7 +189,15 @@ struct SpikeOut<SNN_SPK_U8, 4> {
                                  const bool (&y)[4]) {
         const uint32_t w = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) |
                            (uint32_t(y[3]) << 24);
-        if (active) st_nt(s + t * row_bytes + n0, w);
+        if (active) *reinterpret_cast<uint32_t*>(s + t * row_bytes + n0) = w;
+    }
+};
+
+template <>
+struct SpikeOut<SNN_SPK_U8, 2> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[2]) {
+        if (active) *reinterpret_cast<uint16_t*>(s + t * row_bytes + n0) = (uint16_t(uint32_t(y[0]) | (uint32_t(y[1]) << 8)));
     }
 };
 
@@ -173,7 +205,7 @@ template <>
 struct SpikeOut<SNN_SPK_U8, 1> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[1]) {
-        if (active) st_nt(s + t * row_bytes + n0, uint8_t(y[0]));
+        if (active) s[t * row_bytes + n0] = uint8_t(y[0]);
     }
 };
 
@@ -187,7 +219,20 @@ struct SpikeOut<SNN_SPK_BITS, 4> {
         const int nib = active ? (int(y[0]) | (int(y[1]) << 1) | (int(y[2]) << 2) | (int(y[3]) << 3)) : 0;
         const int other = __builtin_amdgcn_mov_dpp(nib, 0xB1, 0xF, 0xF, false);
         if (((n0 >> 2) & 1) == 0 && n0 < row_bytes * 8)
-            st_nt(s + t * row_bytes + (n0 >> 3), uint8_t(nib | (other << 4)));
+            s[t * row_bytes + (n0 >> 3)] = uint8_t(nib | (other << 4));
+    }
+};
+
+// Bits, 2 neurons per lane: four lanes share a byte; two DPP quad permutations ([1,0,3,2]
+// then [2,3,0,1]) gather it in the first lane of each quad.
+template <>
+struct SpikeOut<SNN_SPK_BITS, 2> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[2]) {
+        int b = active ? (int(y[0]) | (int(y[1]) << 1)) : 0;
+        b |= __builtin_amdgcn_mov_dpp(b, 0xB1, 0xF, 0xF, false) << 2;
+        b |= __builtin_amdgcn_mov_dpp(b, 0x4E, 0xF, 0xF, false) << 4;
+        if (((n0 >> 1) & 3) == 0 && n0 < row_bytes * 8) s[t * row_bytes + (n0 >> 3)] = uint8_t(b);
     }
 };
 
@@ -198,7 +243,7 @@ struct SpikeOut<SNN_SPK_BITS, 1> {
                                  const bool (&y)[1]) {
         const uint64_t word = __ballot(active && y[0]);
         if ((threadIdx.x & (kWave - 1)) == 0 && n0 < row_bytes * 8)
-            st_nt(s + t * row_bytes + (n0 >> 3), word);
+            *reinterpret_cast<uint64_t*>(s + t * row_bytes + (n0 >> 3)) = word;
     }
 };
 
@@ -208,6 +253,9 @@ template <int V>
 __device__ __forceinline__ void store_f32(float* p, const float (&f)[V]) {
     if constexpr (V == 4) {
         const f32x4_t v = {f[0], f[1], f[2], f[3]};
+        st_nt(p, v);
+    } else if constexpr (V == 2) {
+        const f32x2_t v = {f[0], f[1]};
         st_nt(p, v);
     } else {
         st_nt(p, f[0]);
@@ -222,25 +270,40 @@ __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
         f[1] = a[1];
         f[2] = a[2];
         f[3] = a[3];
+    } else if constexpr (V == 2) {
+        const f32x2_t a = ld_nt<f32x2_t>(p);
+        f[0] = a[0];
+        f[1] = a[1];
     } else {
         f[0] = ld_nt<float>(p);
     }
 }
 
 // ------------------------------------------------------------------------------------
-// Forward: one chunk of up to K steps.  FULL chunks skip the per-step bound test.
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL>
-__device__ __forceinline__ void forward_chunk(const LifK& c, int64_t N, int64_t t0, int kn, int64_t n0,
-                                              bool active, const void* __restrict__ x,
-                                              uint8_t* __restrict__ spikes, int64_t row_bytes,
-                                              float* __restrict__ v_out, float (&v)[V], bool (&y)[V]) {
+// Forward and backward bodies.  A chunk is K consecutive steps; only the last chunk of a
+// layer can be shorter (kn < K rows).  Row loads of a chunk are issued together, before
+// the chunk's recurrence, because they do not depend on it.
+template <int IO, int V, int K, bool FULL, bool REV>
+__device__ __forceinline__ void load_rows(typename IoVec<IO, V>::raw (&buf)[K], const void* src, int64_t N,
+                                          int64_t t0, int kn, int64_t n0) {
     using Io = IoVec<IO, V>;
-    typename Io::raw xr[K];
-    if (active) {
+    if constexpr (REV) {
+#pragma unroll
+        for (int i = K - 1; i >= 0; --i)
+            if (FULL || i < kn) buf[i] = Io::load(src, (t0 + i) * N + n0);
+    } else {
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            if (FULL || i < kn) xr[i] = Io::load(x, (t0 + i) * N + n0);
+            if (FULL || i < kn) buf[i] = Io::load(src, (t0 + i) * N + n0);
     }
+}
+
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL>
+__device__ __forceinline__ void forward_rows(const LifK& c, const typename IoVec<IO, V>::raw (&xr)[K], int64_t N,
+                                             int64_t t0, int kn, int64_t n0, bool active,
+                                             uint8_t* __restrict__ spikes, int64_t row_bytes,
+                                             float* __restrict__ v_out, float (&v)[V], bool (&y)[V]) {
+    using Io = IoVec<IO, V>;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
         if (FULL || i < kn) {
@@ -254,13 +317,19 @@ __device__ __forceinline__ void forward_chunk(const LifK& c, int64_t N, int64_t 
 
 // Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
 // N load nothing and report no spikes; they exist only to complete spike-bit words.
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT>
+// Chunks 0 .. n_full-1 have K steps; a last chunk of T % K steps follows when T % K != 0.
+// After every chunk but the last, the membrane is checkpointed to saved[chunk][N].
+// PIPE: double-buffered full chunks -- the next chunk's rows are in flight while the
+// current chunk is computed (for layers with few lanes, where occupancy alone cannot hide
+// the memory latency).
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
 __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
                                                              const void* __restrict__ x,
                                                              uint8_t* __restrict__ spikes,
                                                              int64_t row_bytes,
                                                              float* __restrict__ saved,
                                                              float* __restrict__ v_out) {
+    using raw = typename IoVec<IO, V>::raw;
     const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     const bool active = n0 < N;
     float v[V];
@@ -270,36 +339,45 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
         v[j] = c.rest;  // v^0 = V_rest
         y[j] = false;   // no spike before the first step
     }
-    const int64_t n_chunks = (T + K - 1) / K;
-    for (int64_t ch = 0; ch < n_chunks; ++ch) {
-        const int64_t t0 = ch * K;
-        const int kn = int(T - t0 < K ? T - t0 : K);
-        if (kn == K)
-            forward_chunk<IO, SPK, RESET, V, K, VOUT, true>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
-        else
-            forward_chunk<IO, SPK, RESET, V, K, VOUT, false>(c, N, t0, kn, n0, active, x, spikes, row_bytes, v_out, v, y);
-        if (ch + 1 < n_chunks && active) store_f32<V>(saved + ch * N + n0, v);
+    const int64_t n_full = T / K;
+    const int k_tail = int(T % K);
+    const int64_t last = k_tail ? n_full : n_full - 1;   // index of the last chunk
+    auto full_chunk = [&](const raw (&buf)[K], int64_t ch) {
+        forward_rows<IO, SPK, RESET, V, K, VOUT, true>(c, buf, N, ch * K, K, n0, active, spikes, row_bytes, v_out, v, y);
+        if (ch < last && active) store_f32<V>(saved + ch * N + n0, v);
+    };
+    raw a[K];
+    if constexpr (!PIPE) {
+        for (int64_t ch = 0; ch < n_full; ++ch) {
+            if (active) load_rows<IO, V, K, true, false>(a, x, N, ch * K, K, n0);
+            full_chunk(a, ch);
+        }
+    } else {
+        raw b[K];
+        if (n_full > 0 && active) load_rows<IO, V, K, true, false>(a, x, N, 0, K, n0);
+        for (int64_t ch = 0; ch < n_full; ch += 2) {
+            if (ch + 1 < n_full && active) load_rows<IO, V, K, true, false>(b, x, N, (ch + 1) * K, K, n0);
+            full_chunk(a, ch);
+            if (ch + 1 >= n_full) break;
+            if (ch + 2 < n_full && active) load_rows<IO, V, K, true, false>(a, x, N, (ch + 2) * K, K, n0);
+            full_chunk(b, ch + 1);
+        }
+    }
+    if (k_tail) {
+        if (active) load_rows<IO, V, K, false, false>(a, x, N, n_full * K, k_tail, n0);
+        forward_rows<IO, SPK, RESET, V, K, VOUT, false>(c, a, N, n_full * K, k_tail, n0, active, spikes, row_bytes,
+                                                        v_out, v, y);
     }
 }
 
-// ------------------------------------------------------------------------------------
-// Backward: one chunk.  v/y enter as the state before the chunk's first step; g enters as
-// dL/dv of the step after the chunk and leaves as dL/dv of the chunk's first step.
+// Backward of one chunk.  v/y enter as the state before the chunk's first step; g enters
+// as dL/dv of the step after the chunk and leaves as dL/dv of the chunk's first step.
 template <int IO, int RESET, int V, int K, bool FULL>
-__device__ __forceinline__ void backward_chunk(const LifK& c, int64_t N, int64_t t0, int kn, int64_t n0,
-                                               const void* __restrict__ x, const void* gs, void* gx,
-                                               float (&v)[V], bool (&y)[V], float (&g)[V]) {
+__device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVec<IO, V>::raw (&xr)[K],
+                                              const typename IoVec<IO, V>::raw (&gr)[K], int64_t N, int64_t t0,
+                                              int kn, int64_t n0, void* gx, float (&v)[V], bool (&y)[V],
+                                              float (&g)[V]) {
     using Io = IoVec<IO, V>;
-    typename Io::raw xr[K];
-    typename Io::raw gr[K];
-#pragma unroll
-    for (int i = 0; i < K; ++i)
-        if (FULL || i < kn) xr[i] = Io::load(x, (t0 + i) * N + n0);
-    // dL/dy rows are consumed last-first: issue them in that order
-#pragma unroll
-    for (int i = K - 1; i >= 0; --i)
-        if (FULL || i < kn) gr[i] = Io::load(gs, (t0 + i) * N + n0);
-
     // recompute the chunk's membranes, bit-identical to the forward
     float vs[K][V];
 #pragma unroll
@@ -312,7 +390,6 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, int64_t N, int64_t
             }
         }
     }
-
     // Eq. (3) in reverse time: g^t = dL/dy^t delta^t + (dv^{t+1}/dv^t) g^{t+1}
 #pragma unroll
     for (int i = K - 1; i >= 0; --i) {
@@ -335,7 +412,44 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, int64_t N, int64_t
     }
 }
 
-template <int IO, int RESET, int V, int K>
+// Everything the backward of chunk ch reads: its input rows, its dL/dy rows (issued
+// last-first, the order the reverse pass consumes them) and the state entering it.
+template <int IO, int V, int K>
+struct BwdChunk {
+    typename IoVec<IO, V>::raw x[K];
+    typename IoVec<IO, V>::raw gs[K];
+    float v[V];
+};
+
+template <int IO, int V, int K, bool FULL>
+__device__ __forceinline__ void backward_load(BwdChunk<IO, V, K>& b, const LifK& c, const void* __restrict__ x,
+                                              const float* __restrict__ saved, const void* gs, int64_t N,
+                                              int64_t ch, int kn, int64_t n0) {
+    load_rows<IO, V, K, FULL, false>(b.x, x, N, ch * K, kn, n0);
+    load_rows<IO, V, K, FULL, true>(b.gs, gs, N, ch * K, kn, n0);
+    if (ch == 0) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) b.v[j] = c.rest;
+    } else {
+        load_f32<V>(saved + (ch - 1) * N + n0, b.v);
+    }
+}
+
+template <int IO, int RESET, int V, int K, bool FULL>
+__device__ __forceinline__ void backward_chunk(const LifK& c, const BwdChunk<IO, V, K>& b, int64_t N, int64_t ch,
+                                               int kn, int64_t n0, void* gx, float (&g)[V]) {
+    float v[V];
+    bool y[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        v[j] = b.v[j];
+        y[j] = ch > 0 && b.v[j] >= c.th;  // a checkpoint is a post-step membrane; step 0 has y = 0
+    }
+    backward_rows<IO, RESET, V, K, FULL>(c, b.x, b.gs, N, ch * K, kn, n0, gx, v, y, g);
+}
+
+// Chunks are processed last-first: the short tail chunk (if any), then the full chunks.
+template <int IO, int RESET, int V, int K, bool PIPE>
 __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
                                                               const void* __restrict__ x,
                                                               const float* __restrict__ saved,
@@ -345,48 +459,51 @@ __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T,
     float g[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
-    const int64_t n_chunks = (T + K - 1) / K;
-    for (int64_t ch = n_chunks - 1; ch >= 0; --ch) {
-        const int64_t t0 = ch * K;
-        const int kn = int(T - t0 < K ? T - t0 : K);
-        float v[V];
-        bool y[V];
-        if (ch == 0) {
-#pragma unroll
-            for (int j = 0; j < V; ++j) {
-                v[j] = c.rest;
-                y[j] = false;
-            }
-        } else {
-            load_f32<V>(saved + (ch - 1) * N + n0, v);
-#pragma unroll
-            for (int j = 0; j < V; ++j) y[j] = v[j] >= c.th;
+    const int64_t n_full = T / K;
+    const int k_tail = int(T % K);
+    BwdChunk<IO, V, K> a;
+    if (k_tail) {
+        backward_load<IO, V, K, false>(a, c, x, saved, gs, N, n_full, k_tail, n0);
+        backward_chunk<IO, RESET, V, K, false>(c, a, N, n_full, k_tail, n0, gx, g);
+    }
+    if constexpr (!PIPE) {
+        for (int64_t ch = n_full - 1; ch >= 0; --ch) {
+            backward_load<IO, V, K, true>(a, c, x, saved, gs, N, ch, K, n0);
+            backward_chunk<IO, RESET, V, K, true>(c, a, N, ch, K, n0, gx, g);
         }
-        if (kn == K)
-            backward_chunk<IO, RESET, V, K, true>(c, N, t0, kn, n0, x, gs, gx, v, y, g);
-        else
-            backward_chunk<IO, RESET, V, K, false>(c, N, t0, kn, n0, x, gs, gx, v, y, g);
+    } else {
+        BwdChunk<IO, V, K> b;
+        if (n_full > 0) backward_load<IO, V, K, true>(a, c, x, saved, gs, N, n_full - 1, K, n0);
+        for (int64_t ch = n_full - 1; ch >= 0; ch -= 2) {
+            if (ch >= 1) backward_load<IO, V, K, true>(b, c, x, saved, gs, N, ch - 1, K, n0);
+            backward_chunk<IO, RESET, V, K, true>(c, a, N, ch, K, n0, gx, g);
+            if (ch < 1) break;
+            if (ch >= 2) backward_load<IO, V, K, true>(a, c, x, saved, gs, N, ch - 2, K, n0);
+            backward_chunk<IO, RESET, V, K, true>(c, b, N, ch - 1, K, n0, gx, g);
+        }
     }
 }
 
 // ------------------------------------------------------------------------------------
-// Per-feature gain between stacked layers.  One lane per V neurons walks all T rows.
+// Per-feature gain between stacked layers.  One lane per V neurons walks all T rows,
+// kGlueRows rows of loads in flight at a time.
+constexpr int kGlueRows = 8;
+
+// The spike word holding a lane's V neurons of row t (u8: V bytes; bits: their byte).
 template <int SPK, int V>
-__device__ __forceinline__ void load_spikes(const uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0,
-                                            float (&y)[V]) {
+__device__ __forceinline__ uint32_t spike_word(const uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0) {
     if constexpr (SPK == SNN_SPK_U8) {
-        if constexpr (V == 4) {
-            const uint32_t w = ld_nt<uint32_t>(s + t * row_bytes + n0);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) y[j] = float((w >> (8 * j)) & 0xffu);
-        } else {
-            y[0] = float(ld_nt<uint8_t>(s + t * row_bytes + n0));
-        }
+        if constexpr (V == 4) return *reinterpret_cast<const uint32_t*>(s + t * row_bytes + n0);
+        else return s[t * row_bytes + n0];
     } else {
-        const uint32_t b = ld_nt<uint8_t>(s + t * row_bytes + (n0 >> 3));
-#pragma unroll
-        for (int j = 0; j < V; ++j) y[j] = float((b >> ((n0 + j) & 7)) & 1u);
+        return s[t * row_bytes + (n0 >> 3)];
     }
+}
+
+template <int SPK, int V>
+__device__ __forceinline__ float spike_of(uint32_t w, int64_t n0, int j) {
+    if constexpr (SPK == SNN_SPK_U8) return float((w >> (8 * j)) & 0xffu);
+    else return float((w >> ((n0 + j) & 7)) & 1u);
 }
 
 template <int IO, int SPK, int V>
@@ -400,13 +517,21 @@ __global__ __launch_bounds__(kBlock) void gain_forward_kernel(int64_t T, int64_t
     float gv[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
-    for (int64_t t = 0; t < T; ++t) {
-        float y[V], out[V];
-        load_spikes<SPK, V>(spikes, row_bytes, t, n0, y);
+    auto emit = [&](uint32_t w, int64_t t) {
+        float out[V];
 #pragma unroll
-        for (int j = 0; j < V; ++j) out[j] = gv[j] * y[j];
+        for (int j = 0; j < V; ++j) out[j] = gv[j] * spike_of<SPK, V>(w, n0, j);
         IoVec<IO, V>::store(x_next, t * N + n0, out);
+    };
+    int64_t t0 = 0;
+    for (; t0 + kGlueRows <= T; t0 += kGlueRows) {
+        uint32_t w[kGlueRows];
+#pragma unroll
+        for (int i = 0; i < kGlueRows; ++i) w[i] = spike_word<SPK, V>(spikes, row_bytes, t0 + i, n0);
+#pragma unroll
+        for (int i = 0; i < kGlueRows; ++i) emit(w[i], t0 + i);
     }
+    for (; t0 < T; ++t0) emit(spike_word<SPK, V>(spikes, row_bytes, t0, n0), t0);
 }
 
 template <int IO, int V>
@@ -420,13 +545,21 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
     float gv[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
-    for (int64_t t = 0; t < T; ++t) {
-        const typename Io::raw r = Io::load(gx_next, t * N + n0);
+    auto emit = [&](const typename Io::raw& r, int64_t t) {
         float out[V];
 #pragma unroll
         for (int j = 0; j < V; ++j) out[j] = gv[j] * Io::get(r, j);
         Io::store(gs, t * N + n0, out);
+    };
+    int64_t t0 = 0;
+    for (; t0 + kGlueRows <= T; t0 += kGlueRows) {
+        typename Io::raw r[kGlueRows];
+#pragma unroll
+        for (int i = 0; i < kGlueRows; ++i) r[i] = Io::load(gx_next, (t0 + i) * N + n0);
+#pragma unroll
+        for (int i = 0; i < kGlueRows; ++i) emit(r[i], t0 + i);
     }
+    for (; t0 < T; ++t0) emit(Io::load(gx_next, t0 * N + n0), t0);
 }
 
 // ------------------------------------------------------------------------------------
@@ -472,22 +605,30 @@ int64_t spike_row_bytes(const snn_lif_cfg* c, int64_t N) {
     return c->spk == SNN_SPK_U8 ? N : 8 * ((N + 63) / 64);
 }
 
-// Neurons per lane and steps per chunk.  The same choice drives the forward, the backward
-// and the checkpoint layout, so it depends only on (cfg, N).
+// Neurons per lane (V), steps per chunk (K, also the checkpoint interval) and whether
+// chunks are double-buffered.  The same choice drives the forward, the backward and the
+// checkpoint layout, so it depends only on (cfg, T, N).
 struct Plan {
-    int v;           // neurons per lane: 4 when N % 4 == 0, else 1
-    int k;           // steps per chunk (= checkpoint interval)
+    int v;
+    int k;
+    bool pipe;
     int64_t lanes;   // lanes in the forward grid
     int64_t row_bytes;
 };
 
-constexpr int kChunkVec = 16;
-constexpr int kChunkScalar = 32;
+// Steps per chunk for a lane width: K loads of each streamed tensor are in flight per lane,
+// and the backward keeps K membranes per neuron in VGPRs (twice the buffers when pipelined).
+constexpr int chunk_steps(int v, bool pipe) { return v == 4 ? (pipe ? 8 : 16) : v == 2 ? 16 : 32; }
 
-Plan make_plan(const snn_lif_cfg* c, int64_t N) {
+// Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
+constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
+
+Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
-    p.v = (N % 4 == 0) ? 4 : 1;
-    p.k = p.v == 4 ? kChunkVec : kChunkScalar;
+    p.v = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
+    if (p.v == 4 && N / 4 < kFillLanes) p.v = 2;   // twice the lanes for small layers
+    p.pipe = T > chunk_steps(p.v, false) && N / p.v < 4 * kFillLanes;
+    p.k = chunk_steps(p.v, p.pipe);
     p.row_bytes = spike_row_bytes(c, N);
     const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
     p.lanes = (covered + p.v - 1) / p.v;
@@ -512,27 +653,49 @@ LifK kernel_consts(const snn_lif_cfg* c) {
 
 dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
 
+template <int IO, int SPK, int RESET, int V, bool PIPE>
+snn_status forward_launch_v(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, uint8_t* sp,
+                            float* sv, float* v_out, hipStream_t s) {
+    constexpr int K = chunk_steps(V, PIPE);
+    const dim3 g = grid_for(p.lanes);
+    return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, V, K, true, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
+                 : launch(lif_forward_kernel<IO, SPK, RESET, V, K, false, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
+}
+
 template <int IO, int SPK, int RESET>
 snn_status forward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, void* spikes,
                           void* saved, float* v_out, hipStream_t s) {
     uint8_t* sp = static_cast<uint8_t*>(spikes);
     float* sv = static_cast<float*>(saved);
-    const dim3 g = grid_for(p.lanes);
-    if (p.v == 4)
-        return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec, true>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
-                     : launch(lif_forward_kernel<IO, SPK, RESET, 4, kChunkVec, false>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
-    return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar, true>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
-                 : launch(lif_forward_kernel<IO, SPK, RESET, 1, kChunkScalar, false>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
+    switch (p.v * 2 + int(p.pipe)) {
+        case 8: return forward_launch_v<IO, SPK, RESET, 4, false>(p, k, T, N, x, sp, sv, v_out, s);
+        case 9: return forward_launch_v<IO, SPK, RESET, 4, true>(p, k, T, N, x, sp, sv, v_out, s);
+        case 4: return forward_launch_v<IO, SPK, RESET, 2, false>(p, k, T, N, x, sp, sv, v_out, s);
+        case 5: return forward_launch_v<IO, SPK, RESET, 2, true>(p, k, T, N, x, sp, sv, v_out, s);
+        case 2: return forward_launch_v<IO, SPK, RESET, 1, false>(p, k, T, N, x, sp, sv, v_out, s);
+        default: return forward_launch_v<IO, SPK, RESET, 1, true>(p, k, T, N, x, sp, sv, v_out, s);
+    }
+}
+
+template <int IO, int RESET, int V, bool PIPE>
+snn_status backward_launch_v(const LifK& k, int64_t T, int64_t N, const void* x, const float* sv, const void* gs,
+                             void* gx, hipStream_t s) {
+    constexpr int K = chunk_steps(V, PIPE);
+    return launch(lif_backward_kernel<IO, RESET, V, K, PIPE>, grid_for((N + V - 1) / V), s, k, T, N, x, sv, gs, gx);
 }
 
 template <int IO, int RESET>
 snn_status backward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
                            const void* saved, const void* gs, void* gx, hipStream_t s) {
     const float* sv = static_cast<const float*>(saved);
-    const int64_t lanes = (N + p.v - 1) / p.v;
-    if (p.v == 4)
-        return launch(lif_backward_kernel<IO, RESET, 4, kChunkVec>, grid_for(lanes), s, k, T, N, x, sv, gs, gx);
-    return launch(lif_backward_kernel<IO, RESET, 1, kChunkScalar>, grid_for(lanes), s, k, T, N, x, sv, gs, gx);
+    switch (p.v * 2 + int(p.pipe)) {
+        case 8: return backward_launch_v<IO, RESET, 4, false>(k, T, N, x, sv, gs, gx, s);
+        case 9: return backward_launch_v<IO, RESET, 4, true>(k, T, N, x, sv, gs, gx, s);
+        case 4: return backward_launch_v<IO, RESET, 2, false>(k, T, N, x, sv, gs, gx, s);
+        case 5: return backward_launch_v<IO, RESET, 2, true>(k, T, N, x, sv, gs, gx, s);
+        case 2: return backward_launch_v<IO, RESET, 1, false>(k, T, N, x, sv, gs, gx, s);
+        default: return backward_launch_v<IO, RESET, 1, true>(k, T, N, x, sv, gs, gx, s);
+    }
 }
 
 }  // namespace
@@ -566,7 +729,7 @@ snn_status snn_lif_saved_bytes(const snn_lif_cfg* cfg, int64_t T, int64_t N, siz
     if (st != SNN_OK) return st;
     if (bytes == nullptr) return SNN_E_NULL;
     if ((st = check_shape(T, N)) != SNN_OK) return st;
-    *bytes = (T == 0 || N == 0) ? 0 : size_t(saved_bytes(make_plan(cfg, N), T, N));
+    *bytes = (T == 0 || N == 0) ? 0 : size_t(saved_bytes(make_plan(cfg, T, N), T, N));
     return SNN_OK;
 }
 
@@ -576,7 +739,7 @@ snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const v
     if (st != SNN_OK) return st;
     if ((st = check_shape(T, N)) != SNN_OK) return st;
     if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, N);
+    const Plan p = make_plan(cfg, T, N);
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (x == nullptr || spikes == nullptr || (need_saved && saved == nullptr)) return SNN_E_NULL;
     if (!aligned(x) || !aligned(spikes) || (saved && !aligned(saved)) || (v_out && !aligned(v_out)))
@@ -604,7 +767,7 @@ snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const 
     if (st != SNN_OK) return st;
     if ((st = check_shape(T, N)) != SNN_OK) return st;
     if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, N);
+    const Plan p = make_plan(cfg, T, N);
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (x == nullptr || grad_s == nullptr || grad_x == nullptr || (need_saved && saved == nullptr))
         return SNN_E_NULL;

@@ -51,15 +51,21 @@ def test_size_formulas(nat):
     for N in (0, 1, 63, 64, 65, 1000, 8388608):
         assert nat.snn_spike_row_bytes(cfg8, N) == N
         assert nat.snn_spike_row_bytes(cfgb, N) == 8 * ((N + 63) // 64)
-    # checkpoints: one fp32 row per completed chunk except the last; 16-step chunks when
-    # N % 4 == 0, 32-step chunks otherwise
+    # checkpoints: one fp32 row of N per chunk boundary; chunks hold 8 to 32 steps depending
+    # on the lane plan, so short layers need none and the size grows with T
     for io in ("f32", "bf16"):
         c = nat.make_cfg(0.5, 1.0, io=io)
-        assert nat.snn_lif_saved_bytes(c, 16, 4096) == 0
-        assert nat.snn_lif_saved_bytes(c, 17, 4096) == 4096 * 4
+        for N in (1, 4097, 4096, 131072, 524288, 1 << 24):
+            sizes = [nat.snn_lif_saved_bytes(c, T, N) for T in range(0, 300, 7)]
+            assert all(sz % (4 * N) == 0 for sz in sizes)
+            assert sizes == sorted(sizes)
+            for T in (1, 8, 16):
+                assert nat.snn_lif_saved_bytes(c, T, N) == 0
+            for T in (33, 100, 256):
+                chunks = nat.snn_lif_saved_bytes(c, T, N) // (4 * N) + 1
+                assert -(-T // 32) <= chunks <= -(-T // 8)
+        # large layers use 16-step chunks
         assert nat.snn_lif_saved_bytes(c, 256, 1 << 24) == 15 * (1 << 24) * 4
-        assert nat.snn_lif_saved_bytes(c, 32, 4097) == 0
-        assert nat.snn_lif_saved_bytes(c, 65, 4097) == 2 * 4097 * 4
         assert nat.snn_lif_saved_bytes(c, 0, 4096) == 0
         assert nat.snn_lif_saved_bytes(c, 100, 0) == 0
 

@@ -209,3 +209,25 @@ def test_gain_glue(H, io, spk, T, B, F):
     ref, bound = H.oracle.gain_backward(gxn, np.abs(gxn), gain, B, F)
     rtol = H.parity.RTOL_BF16 if io == "bf16" else 1e-7
     assert np.all(np.abs(H.to_host_f32(gs) - ref) <= rtol * bound)
+
+
+# Shapes that reach every lane/chunk plan of the library (lanes per neuron group V in
+# {4, 2, 1}, single or multi-chunk, double-buffered or not, with a short tail chunk), run
+# in full on the GPU and checked on sampled neuron columns.
+PLAN_SHAPES = [
+    (16, 1 << 20),          # 4 neurons per lane, one chunk
+    (40, (1 << 20) + 4),    # 4 per lane, double-buffered 8-step chunks, tail
+    (40, 1 << 22),          # 4 per lane, 16-step chunks, tail
+    (16, 524290),           # 2 per lane, one chunk
+    (40, 600002),           # 2 per lane, double-buffered, tail
+    (40, 262145),           # 1 per lane (odd N), double-buffered 32-step chunks, tail
+    (20, (1 << 20) + 1),    # 1 per lane, one chunk
+]
+
+
+@pytest.mark.parametrize("T,N", PLAN_SHAPES, ids=lambda v: str(v))
+@pytest.mark.parametrize("reset,io,spk", COMBOS, ids=lambda v: str(v))
+def test_plans(H, T, N, reset, io, spk):
+    w = _workload(H, T, N, "k05", reset, io, spk, seed=77 + T + N)
+    rep = H.check_sampled(w, 1 << 12, v_out=True)
+    assert rep.ok(), str(rep)
