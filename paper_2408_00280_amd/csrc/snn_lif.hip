@@ -24,6 +24,7 @@
 #include <cmath>
 #include <cstdint>
 #include <tuple>
+#include <type_traits>
 #include <utility>
 
 #include "snn_lif.h"
@@ -281,8 +282,16 @@ __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
 
 // ------------------------------------------------------------------------------------
 // Forward and backward bodies.  A chunk is K consecutive steps; only the last chunk of a
-// layer can be shorter (kn < K rows).  Row loads of a chunk are issued together, before
-// the chunk's recurrence, because they do not depend on it.
+// layer can be shorter (T % K rows).  Row loads of a chunk are issued together, before the
+// chunk's recurrence, because they do not depend on it.
+//
+// On gfx9-family GPUs one in-order counter (vmcnt) covers every outstanding vector load
+// AND store, and the compiler's wait before a use is only as precise as the control flow
+// allows: a load or store under a branch makes the merged count conservative, and then a
+// wait for an old row also waits for younger loads.  So: workgroups whose lanes are all in
+// range run a path with no per-lane guards (ALL = true), checkpoint loads are issued before
+// the row loads they precede in use, and double-buffered loops peel their first iteration
+// so that the loop body issues every load unconditionally.
 template <int IO, int V, int K, bool FULL, bool REV>
 __device__ __forceinline__ void load_rows(typename IoVec<IO, V>::raw (&buf)[K], const void* src, int64_t N,
                                           int64_t t0, int kn, int64_t n0) {
@@ -298,40 +307,36 @@ __device__ __forceinline__ void load_rows(typename IoVec<IO, V>::raw (&buf)[K], 
     }
 }
 
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL>
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL, bool ALL>
 __device__ __forceinline__ void forward_rows(const LifK& c, const typename IoVec<IO, V>::raw (&xr)[K], int64_t N,
                                              int64_t t0, int kn, int64_t n0, bool active,
                                              uint8_t* __restrict__ spikes, int64_t row_bytes,
                                              float* __restrict__ v_out, float (&v)[V], bool (&y)[V]) {
     using Io = IoVec<IO, V>;
+    const bool on = ALL || active;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
         if (FULL || i < kn) {
 #pragma unroll
-            for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], active ? Io::get(xr[i], j) : 0.0f);
-            SpikeOut<SPK, V>::store(spikes, row_bytes, t0 + i, n0, active, y);
-            if (VOUT && active) store_f32<V>(v_out + (t0 + i) * N + n0, v);
+            for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], on ? Io::get(xr[i], j) : 0.0f);
+            SpikeOut<SPK, V>::store(spikes, row_bytes, t0 + i, n0, on, y);
+            if (VOUT && on) store_f32<V>(v_out + (t0 + i) * N + n0, v);
         }
     }
 }
 
-// Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
-// N load nothing and report no spikes; they exist only to complete spike-bit words.
-// Chunks 0 .. n_full-1 have K steps; a last chunk of T % K steps follows when T % K != 0.
-// After every chunk but the last, the membrane is checkpointed to saved[chunk][N].
-// PIPE: double-buffered full chunks -- the next chunk's rows are in flight while the
-// current chunk is computed (for layers with few lanes, where occupancy alone cannot hide
-// the memory latency).
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
-__global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
-                                                             const void* __restrict__ x,
-                                                             uint8_t* __restrict__ spikes,
-                                                             int64_t row_bytes,
-                                                             float* __restrict__ saved,
-                                                             float* __restrict__ v_out) {
+// Forward of one workgroup's lanes.  Chunks 0 .. n_full-1 have K steps; a tail chunk of
+// T % K steps follows when T % K != 0.  After every chunk but the last the membrane is
+// checkpointed to saved[chunk][N].  PIPE: double-buffered chunks -- the next chunk's rows
+// are in flight while the current chunk is computed (for layers with few lanes, where
+// occupancy alone cannot hide the memory latency).
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE, bool ALL>
+__device__ __forceinline__ void forward_lanes(const LifK& c, int64_t T, int64_t N, int64_t n0,
+                                              const void* __restrict__ x, uint8_t* __restrict__ spikes,
+                                              int64_t row_bytes, float* __restrict__ saved,
+                                              float* __restrict__ v_out) {
     using raw = typename IoVec<IO, V>::raw;
-    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
-    const bool active = n0 < N;
+    const bool active = ALL || n0 < N;
     float v[V];
     bool y[V];
 #pragma unroll
@@ -342,32 +347,77 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
     const int64_t n_full = T / K;
     const int k_tail = int(T % K);
     const int64_t last = k_tail ? n_full : n_full - 1;   // index of the last chunk
-    auto full_chunk = [&](const raw (&buf)[K], int64_t ch) {
-        forward_rows<IO, SPK, RESET, V, K, VOUT, true>(c, buf, N, ch * K, K, n0, active, spikes, row_bytes, v_out, v, y);
-        if (ch < last && active) store_f32<V>(saved + ch * N + n0, v);
+    // The scheduler must not move a chunk's compute across the batch of loads that
+    // precedes it: that would change the outstanding-operation count between loop entry
+    // and back-edge and make the compiler's waits conservative.
+    auto load = [&](raw (&buf)[K], int64_t ch) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (ALL || active) load_rows<IO, V, K, true, false>(buf, x, N, ch * K, K, n0);
+        __builtin_amdgcn_sched_barrier(0);
     };
+    // CKPT: 1 = this chunk is never the last (checkpoint unconditionally), 0 = test at run time
+    auto step = [&](const raw (&buf)[K], int64_t ch, auto ckpt) {
+        forward_rows<IO, SPK, RESET, V, K, VOUT, true, ALL>(c, buf, N, ch * K, K, n0, active, spikes, row_bytes,
+                                                            v_out, v, y);
+        if ((decltype(ckpt)::value || ch < last) && (ALL || active)) store_f32<V>(saved + ch * N + n0, v);
+    };
+    constexpr std::true_type not_last{};
+    constexpr std::false_type maybe_last{};
     raw a[K];
     if constexpr (!PIPE) {
         for (int64_t ch = 0; ch < n_full; ++ch) {
-            if (active) load_rows<IO, V, K, true, false>(a, x, N, ch * K, K, n0);
-            full_chunk(a, ch);
+            load(a, ch);
+            step(a, ch, maybe_last);
         }
-    } else {
+    } else if (n_full > 0) {
         raw b[K];
-        if (n_full > 0 && active) load_rows<IO, V, K, true, false>(a, x, N, 0, K, n0);
-        for (int64_t ch = 0; ch < n_full; ch += 2) {
-            if (ch + 1 < n_full && active) load_rows<IO, V, K, true, false>(b, x, N, (ch + 1) * K, K, n0);
-            full_chunk(a, ch);
-            if (ch + 1 >= n_full) break;
-            if (ch + 2 < n_full && active) load_rows<IO, V, K, true, false>(a, x, N, (ch + 2) * K, K, n0);
-            full_chunk(b, ch + 1);
+        load(a, 0);
+        if (n_full == 1) {
+            step(a, 0, maybe_last);
+        } else {
+            // Entering the loop, chunk ch is in flight in b and a is free: the same state
+            // each iteration ends in, so the buffers keep their roles and every load and
+            // store in the loop body is unconditional.
+            load(b, 1);
+            step(a, 0, not_last);
+            int64_t ch = 1;
+            for (; ch + 2 < n_full; ch += 2) {
+                load(a, ch + 1);
+                step(b, ch, not_last);
+                load(b, ch + 2);
+                step(a, ch + 1, not_last);
+            }
+            if (ch + 1 < n_full) {
+                load(a, ch + 1);
+                step(b, ch, not_last);
+                step(a, ch + 1, maybe_last);
+            } else {
+                step(b, ch, maybe_last);
+            }
         }
     }
     if (k_tail) {
-        if (active) load_rows<IO, V, K, false, false>(a, x, N, n_full * K, k_tail, n0);
-        forward_rows<IO, SPK, RESET, V, K, VOUT, false>(c, a, N, n_full * K, k_tail, n0, active, spikes, row_bytes,
-                                                        v_out, v, y);
+        if (ALL || active) load_rows<IO, V, K, false, false>(a, x, N, n_full * K, k_tail, n0);
+        forward_rows<IO, SPK, RESET, V, K, VOUT, false, ALL>(c, a, N, n_full * K, k_tail, n0, active, spikes,
+                                                             row_bytes, v_out, v, y);
     }
+}
+
+// Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
+// N load nothing and report no spikes; they exist only to complete spike-bit words.
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
+__global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
+                                                             const void* __restrict__ x,
+                                                             uint8_t* __restrict__ spikes,
+                                                             int64_t row_bytes,
+                                                             float* __restrict__ saved,
+                                                             float* __restrict__ v_out) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    if (first + kBlock * V <= N)
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, T, N, n0, x, spikes, row_bytes, saved, v_out);
+    else
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, T, N, n0, x, spikes, row_bytes, saved, v_out);
 }
 
 // Backward of one chunk.  v/y enter as the state before the chunk's first step; g enters
@@ -412,8 +462,8 @@ __device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVe
     }
 }
 
-// Everything the backward of chunk ch reads: its input rows, its dL/dy rows (issued
-// last-first, the order the reverse pass consumes them) and the state entering it.
+// Everything the backward of chunk ch reads: the state entering it (loaded first), its
+// input rows, and its dL/dy rows (issued last-first, the order the reverse pass uses them).
 template <int IO, int V, int K>
 struct BwdChunk {
     typename IoVec<IO, V>::raw x[K];
@@ -421,18 +471,22 @@ struct BwdChunk {
     float v[V];
 };
 
-template <int IO, int V, int K, bool FULL>
+// ALWAYS: the layer has a checkpoint row, so the state is loaded unconditionally (chunk 0
+// reads row 0 and then takes V_rest instead), keeping the caller's loop free of branches.
+template <int IO, int V, int K, bool FULL, bool ALWAYS>
 __device__ __forceinline__ void backward_load(BwdChunk<IO, V, K>& b, const LifK& c, const void* __restrict__ x,
                                               const float* __restrict__ saved, const void* gs, int64_t N,
                                               int64_t ch, int kn, int64_t n0) {
-    load_rows<IO, V, K, FULL, false>(b.x, x, N, ch * K, kn, n0);
-    load_rows<IO, V, K, FULL, true>(b.gs, gs, N, ch * K, kn, n0);
-    if (ch == 0) {
+    if (ALWAYS) {
+        load_f32<V>(saved + (ch > 0 ? ch - 1 : 0) * N + n0, b.v);
+    } else if (ch == 0) {
 #pragma unroll
         for (int j = 0; j < V; ++j) b.v[j] = c.rest;
     } else {
         load_f32<V>(saved + (ch - 1) * N + n0, b.v);
     }
+    load_rows<IO, V, K, FULL, false>(b.x, x, N, ch * K, kn, n0);
+    load_rows<IO, V, K, FULL, true>(b.gs, gs, N, ch * K, kn, n0);
 }
 
 template <int IO, int RESET, int V, int K, bool FULL>
@@ -442,7 +496,7 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, const BwdChunk<IO,
     bool y[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-        v[j] = b.v[j];
+        v[j] = ch > 0 ? b.v[j] : c.rest;
         y[j] = ch > 0 && b.v[j] >= c.th;  // a checkpoint is a post-step membrane; step 0 has y = 0
     }
     backward_rows<IO, RESET, V, K, FULL>(c, b.x, b.gs, N, ch * K, kn, n0, gx, v, y, g);
@@ -450,12 +504,9 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, const BwdChunk<IO,
 
 // Chunks are processed last-first: the short tail chunk (if any), then the full chunks.
 template <int IO, int RESET, int V, int K, bool PIPE>
-__global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
-                                                              const void* __restrict__ x,
-                                                              const float* __restrict__ saved,
-                                                              const void* gs, void* gx) {
-    const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
-    if (n0 >= N) return;
+__device__ __forceinline__ void backward_lanes(const LifK& c, int64_t T, int64_t N, int64_t n0,
+                                               const void* __restrict__ x, const float* __restrict__ saved,
+                                               const void* gs, void* gx) {
     float g[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
@@ -463,25 +514,58 @@ __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T,
     const int k_tail = int(T % K);
     BwdChunk<IO, V, K> a;
     if (k_tail) {
-        backward_load<IO, V, K, false>(a, c, x, saved, gs, N, n_full, k_tail, n0);
+        backward_load<IO, V, K, false, false>(a, c, x, saved, gs, N, n_full, k_tail, n0);
         backward_chunk<IO, RESET, V, K, false>(c, a, N, n_full, k_tail, n0, gx, g);
     }
+    auto load = [&](BwdChunk<IO, V, K>& buf, int64_t ch) {
+        __builtin_amdgcn_sched_barrier(0);
+        backward_load<IO, V, K, true, PIPE>(buf, c, x, saved, gs, N, ch, K, n0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto step = [&](const BwdChunk<IO, V, K>& buf, int64_t ch) {
+        backward_chunk<IO, RESET, V, K, true>(c, buf, N, ch, K, n0, gx, g);
+    };
     if constexpr (!PIPE) {
         for (int64_t ch = n_full - 1; ch >= 0; --ch) {
-            backward_load<IO, V, K, true>(a, c, x, saved, gs, N, ch, K, n0);
-            backward_chunk<IO, RESET, V, K, true>(c, a, N, ch, K, n0, gx, g);
+            load(a, ch);
+            step(a, ch);
         }
-    } else {
+    } else if (n_full > 0) {
         BwdChunk<IO, V, K> b;
-        if (n_full > 0) backward_load<IO, V, K, true>(a, c, x, saved, gs, N, n_full - 1, K, n0);
-        for (int64_t ch = n_full - 1; ch >= 0; ch -= 2) {
-            if (ch >= 1) backward_load<IO, V, K, true>(b, c, x, saved, gs, N, ch - 1, K, n0);
-            backward_chunk<IO, RESET, V, K, true>(c, a, N, ch, K, n0, gx, g);
-            if (ch < 1) break;
-            if (ch >= 2) backward_load<IO, V, K, true>(a, c, x, saved, gs, N, ch - 2, K, n0);
-            backward_chunk<IO, RESET, V, K, true>(c, b, N, ch - 1, K, n0, gx, g);
+        load(a, n_full - 1);
+        if (n_full == 1) {
+            step(a, 0);
+        } else {
+            // as in the forward: entering the loop, chunk ch is in flight in b, a is free
+            load(b, n_full - 2);
+            step(a, n_full - 1);
+            int64_t ch = n_full - 2;
+            for (; ch >= 2; ch -= 2) {
+                load(a, ch - 1);
+                step(b, ch);
+                load(b, ch - 2);
+                step(a, ch - 1);
+            }
+            if (ch >= 1) {
+                load(a, ch - 1);
+                step(b, ch);
+                step(a, ch - 1);
+            } else {
+                step(b, ch);
+            }
         }
     }
+}
+
+template <int IO, int RESET, int V, int K, bool PIPE>
+__global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
+                                                              const void* __restrict__ x,
+                                                              const float* __restrict__ saved,
+                                                              const void* gs, void* gx) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    if (first + kBlock * V > N && n0 >= N) return;
+    backward_lanes<IO, RESET, V, K, PIPE>(c, T, N, n0, x, saved, gs, gx);
 }
 
 // ------------------------------------------------------------------------------------
