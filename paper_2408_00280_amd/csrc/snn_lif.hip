@@ -124,6 +124,18 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
 template <>
+struct IoVec<SNN_IO_BF16, 8> {
+    using raw = u32x4_t;
+    __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const uint16_t*>(b) + i); }
+    __device__ static float get(const raw& r, int j) { return (j & 1) ? bf16_hi(r[j >> 1]) : bf16_lo(r[j >> 1]); }
+    __device__ static void store(void* b, int64_t i, const float (&f)[8]) {
+        const raw w = {pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                       pack_bf16x2(f[6], f[7])};
+        st_nt(static_cast<uint16_t*>(b) + i, w);
+    }
+};
+
+template <>
 struct IoVec<SNN_IO_BF16, 4> {
     using raw = u32x2_t;
     __device__ static raw load(const void* b, int64_t i) { return ld_nt<raw>(static_cast<const uint16_t*>(b) + i); }
@@ -195,6 +207,17 @@ struct SpikeOut<SNN_SPK_U8, 4> {
 };
 
 template <>
+struct SpikeOut<SNN_SPK_U8, 8> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[8]) {
+        uint2 w;
+        w.x = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) | (uint32_t(y[3]) << 24);
+        w.y = uint32_t(y[4]) | (uint32_t(y[5]) << 8) | (uint32_t(y[6]) << 16) | (uint32_t(y[7]) << 24);
+        if (active) *reinterpret_cast<uint2*>(s + t * row_bytes + n0) = w;
+    }
+};
+
+template <>
 struct SpikeOut<SNN_SPK_U8, 2> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[2]) {
@@ -237,6 +260,18 @@ struct SpikeOut<SNN_SPK_BITS, 2> {
     }
 };
 
+// Bits, 8 neurons per lane: each lane owns one byte of the row.
+template <>
+struct SpikeOut<SNN_SPK_BITS, 8> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[8]) {
+        uint32_t b = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) b |= uint32_t(y[j]) << j;
+        if (n0 < row_bytes * 8) s[t * row_bytes + (n0 >> 3)] = uint8_t(active ? b : 0u);
+    }
+};
+
 // Bits, 1 neuron per lane: one wave64 ballot is one 64-bit word of the row.
 template <>
 struct SpikeOut<SNN_SPK_BITS, 1> {
@@ -252,7 +287,11 @@ struct SpikeOut<SNN_SPK_BITS, 1> {
 // fp32 rows of V neurons (checkpoints and the optional membrane output).
 template <int V>
 __device__ __forceinline__ void store_f32(float* p, const float (&f)[V]) {
-    if constexpr (V == 4) {
+    if constexpr (V == 8) {
+        const f32x4_t lo = {f[0], f[1], f[2], f[3]}, hi = {f[4], f[5], f[6], f[7]};
+        st_nt(p, lo);
+        st_nt(p + 4, hi);
+    } else if constexpr (V == 4) {
         const f32x4_t v = {f[0], f[1], f[2], f[3]};
         st_nt(p, v);
     } else if constexpr (V == 2) {
@@ -689,33 +728,39 @@ int64_t spike_row_bytes(const snn_lif_cfg* c, int64_t N) {
     return c->spk == SNN_SPK_U8 ? N : 8 * ((N + 63) / 64);
 }
 
-// Neurons per lane (V), steps per chunk (K, also the checkpoint interval) and whether
-// chunks are double-buffered.  The same choice drives the forward, the backward and the
-// checkpoint layout, so it depends only on (cfg, T, N).
+// Neurons per lane in the forward (vf) and the backward (vb), steps per chunk (K, also the
+// checkpoint interval, sized by the backward's register budget) and whether chunks are
+// double-buffered.  The same choice drives both kernels and the checkpoint layout (which
+// does not depend on the lane widths), so it depends only on (cfg, T, N).
 struct Plan {
-    int v;
+    int vf;
+    int vb;
     int k;
     bool pipe;
     int64_t lanes;   // lanes in the forward grid
     int64_t row_bytes;
 };
 
-// Steps per chunk for a lane width: K loads of each streamed tensor are in flight per lane,
-// and the backward keeps K membranes per neuron in VGPRs (twice the buffers when pipelined).
-constexpr int chunk_steps(int v, bool pipe) { return v == 4 ? (pipe ? 8 : 16) : v == 2 ? 16 : 32; }
+// Steps per chunk: the backward keeps K membranes per neuron in VGPRs plus K rows of x and
+// dL/dy (twice the rows when double-buffered); bf16 rows take half the registers.
+constexpr int chunk_steps(int io, int v, bool pipe) {
+    return v == 4 ? (pipe && io == SNN_IO_F32 ? 8 : 16) : v == 2 ? 16 : 32;
+}
 
 // Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
 constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 
 Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
-    p.v = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
-    if (p.v == 4 && N / 4 < kFillLanes) p.v = 2;   // twice the lanes for small layers
-    p.pipe = T > chunk_steps(p.v, false) && N / p.v < 4 * kFillLanes;
-    p.k = chunk_steps(p.v, p.pipe);
+    p.vb = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
+    if (p.vb == 4 && N / 4 < kFillLanes) p.vb = 2;   // twice the lanes for small layers
+    p.pipe = T > chunk_steps(c->io, p.vb, false) && N / p.vb < 4 * kFillLanes;
+    p.k = chunk_steps(c->io, p.vb, p.pipe);
+    // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
+    p.vf = (c->io == SNN_IO_BF16 && p.vb == 4 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
     p.row_bytes = spike_row_bytes(c, N);
     const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
-    p.lanes = (covered + p.v - 1) / p.v;
+    p.lanes = (covered + p.vf - 1) / p.vf;
     return p;
 }
 
@@ -737,34 +782,41 @@ LifK kernel_consts(const snn_lif_cfg* c) {
 
 dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
 
-template <int IO, int SPK, int RESET, int V, bool PIPE>
+template <int IO, int SPK, int RESET, int V, int K, bool PIPE>
 snn_status forward_launch_v(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, uint8_t* sp,
                             float* sv, float* v_out, hipStream_t s) {
-    constexpr int K = chunk_steps(V, PIPE);
     const dim3 g = grid_for(p.lanes);
     return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, V, K, true, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
                  : launch(lif_forward_kernel<IO, SPK, RESET, V, K, false, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
 }
 
+// (vf, vb, pipe) combinations the planner produces.
 template <int IO, int SPK, int RESET>
 snn_status forward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, void* spikes,
                           void* saved, float* v_out, hipStream_t s) {
     uint8_t* sp = static_cast<uint8_t*>(spikes);
     float* sv = static_cast<float*>(saved);
-    switch (p.v * 2 + int(p.pipe)) {
-        case 8: return forward_launch_v<IO, SPK, RESET, 4, false>(p, k, T, N, x, sp, sv, v_out, s);
-        case 9: return forward_launch_v<IO, SPK, RESET, 4, true>(p, k, T, N, x, sp, sv, v_out, s);
-        case 4: return forward_launch_v<IO, SPK, RESET, 2, false>(p, k, T, N, x, sp, sv, v_out, s);
-        case 5: return forward_launch_v<IO, SPK, RESET, 2, true>(p, k, T, N, x, sp, sv, v_out, s);
-        case 2: return forward_launch_v<IO, SPK, RESET, 1, false>(p, k, T, N, x, sp, sv, v_out, s);
-        default: return forward_launch_v<IO, SPK, RESET, 1, true>(p, k, T, N, x, sp, sv, v_out, s);
+    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
+    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
+    if constexpr (IO == SNN_IO_BF16) {
+        if (p.vf == 8)
+            return p.pipe ? forward_launch_v<IO, SPK, RESET, 8, K4p, true>(p, k, T, N, x, sp, sv, v_out, s)
+                          : forward_launch_v<IO, SPK, RESET, 8, K4, false>(p, k, T, N, x, sp, sv, v_out, s);
+    }
+    switch (p.vf * 2 + int(p.pipe)) {
+        case 8: return forward_launch_v<IO, SPK, RESET, 4, K4, false>(p, k, T, N, x, sp, sv, v_out, s);
+        case 9: return forward_launch_v<IO, SPK, RESET, 4, K4p, true>(p, k, T, N, x, sp, sv, v_out, s);
+        case 4: return forward_launch_v<IO, SPK, RESET, 2, K2, false>(p, k, T, N, x, sp, sv, v_out, s);
+        case 5: return forward_launch_v<IO, SPK, RESET, 2, K2, true>(p, k, T, N, x, sp, sv, v_out, s);
+        case 2: return forward_launch_v<IO, SPK, RESET, 1, K1, false>(p, k, T, N, x, sp, sv, v_out, s);
+        default: return forward_launch_v<IO, SPK, RESET, 1, K1, true>(p, k, T, N, x, sp, sv, v_out, s);
     }
 }
 
 template <int IO, int RESET, int V, bool PIPE>
 snn_status backward_launch_v(const LifK& k, int64_t T, int64_t N, const void* x, const float* sv, const void* gs,
                              void* gx, hipStream_t s) {
-    constexpr int K = chunk_steps(V, PIPE);
+    constexpr int K = chunk_steps(IO, V, PIPE);
     return launch(lif_backward_kernel<IO, RESET, V, K, PIPE>, grid_for((N + V - 1) / V), s, k, T, N, x, sv, gs, gx);
 }
 
@@ -772,7 +824,7 @@ template <int IO, int RESET>
 snn_status backward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
                            const void* saved, const void* gs, void* gx, hipStream_t s) {
     const float* sv = static_cast<const float*>(saved);
-    switch (p.v * 2 + int(p.pipe)) {
+    switch (p.vb * 2 + int(p.pipe)) {
         case 8: return backward_launch_v<IO, RESET, 4, false>(k, T, N, x, sv, gs, gx, s);
         case 9: return backward_launch_v<IO, RESET, 4, true>(k, T, N, x, sv, gs, gx, s);
         case 4: return backward_launch_v<IO, RESET, 2, false>(k, T, N, x, sv, gs, gx, s);
