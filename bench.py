@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, published
-KERNEL_SRC = os.path.join(ROOT, "paper_2408_00280_amd", "csrc", "snn_lif.hip")
+KERNEL_SRC_DIR = os.path.join(ROOT, "paper_2408_00280_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
 ROTATE_BYTES = 1 << 30
 
@@ -44,8 +44,12 @@ def bytes_per_nts(w):
 
 
 def source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel sources (every file under csrc/, in name order)."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_SRC_DIR)):
+        with open(os.path.join(KERNEL_SRC_DIR, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel_tag: str, workload_tag: str):

@@ -58,10 +58,12 @@ typedef enum {
 } snn_io;
 
 typedef enum {
-    SNN_SPK_U8 = 0,  /* one byte per neuron (0 or 1): row t at byte t*N */
-    SNN_SPK_BITS = 1 /* one bit per neuron: neuron n of row t is bit (n & 7) of byte
-                        t*row_bytes + (n >> 3), row_bytes = 8*ceil(N/64) (whole little-endian
-                        64-bit words), padding bits are written as 0 */
+    SNN_SPK_U8 = 0,   /* one byte per neuron (0 or 1): row t at byte t*N */
+    SNN_SPK_BITS = 1, /* one bit per neuron: neuron n of row t is bit (n & 7) of byte
+                         t*row_bytes + (n >> 3), row_bytes = 8*ceil(N/64) (whole little-endian
+                         64-bit words), padding bits are written as 0 */
+    SNN_SPK_IO = 2    /* 0.0 / 1.0 in the I/O dtype, [T][N] like x: the layer's output as a
+                         tensor a following ANN operator can consume directly */
 } snn_spk;
 
 typedef struct {
@@ -75,7 +77,8 @@ typedef struct {
     int32_t spk;   /* snn_spk */
 } snn_lif_cfg;
 
-/* Bytes of one spike row for N neurons in cfg->spk's format (N, or 8*ceil(N/64)).
+/* Bytes of one spike row for N neurons in cfg->spk's format (N, 8*ceil(N/64), or N times
+ * the I/O element size).
  * Host-only; SNN_E_NULL / SNN_E_PARAM / SNN_E_SHAPE on bad arguments. */
 snn_status snn_spike_row_bytes(const snn_lif_cfg *cfg, int64_t N, size_t *bytes);
 

@@ -1,0 +1,63 @@
+"""The fused LIF layer as a torch autograd function and module.
+
+This is the programming model of the paper's Listing 1 (a ``FusedLIF`` autograd function
+wrapping the fused forward and backward kernels, and a ``LIFLayer`` module to drop into
+``torch.nn.Sequential`` next to ANN operators), with two differences: the state the
+backward needs (the input current and the membrane checkpoints) is saved explicitly, and
+the backward returns no gradient for the hyper-parameters.
+
+Inputs are time-major, ``x[T, ...]``, float32 or bfloat16; the output is the spike train
+``y[T, ...]`` as 0/1 values of the same dtype.  The arithmetic runs in the HIP kernels;
+torch allocates and orders the work on its current stream.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import layer
+
+_IO = {torch.float32: "f32", torch.bfloat16: "bf16"}
+
+
+class FusedLIF(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x: torch.Tensor, cfg: layer.LifConfig):
+        if x.dtype not in _IO or cfg.io != _IO[x.dtype] or cfg.spk != "io":
+            raise TypeError("FusedLIF takes float32/bfloat16 input and a cfg with io matching it and spk='io'")
+        xc = x.contiguous()
+        T = xc.shape[0]
+        x2 = xc.view(T, -1)
+        spikes, saved, _ = layer.forward(cfg, x2)
+        ctx.save_for_backward(x2, saved)
+        ctx.cfg = cfg
+        ctx.shape = x.shape
+        return spikes.view(x.shape)
+
+    @staticmethod
+    def backward(ctx, grad_y: torch.Tensor):
+        x2, saved = ctx.saved_tensors
+        g = grad_y.to(x2.dtype).contiguous().view(x2.shape)
+        grad_x = layer.backward(ctx.cfg, x2, saved, g)
+        return grad_x.view(ctx.shape), None
+
+
+class LIFLayer(torch.nn.Module):
+    """Leaky integrate-and-fire neurons over the leading (time) axis of the input.
+
+    decay is k_tau of Eq. (1) (k_tau = 1 - 1/tau), v_th the threshold of Eq. (2), v_reset
+    V_rest (initial membrane and hard-reset value), alpha the sigmoid-surrogate sharpness,
+    reset "hard" (Eq. (1)) or "soft" (subtract the threshold)."""
+
+    def __init__(self, decay: float, v_th: float, v_reset: float = 0.0, alpha: float = 4.0, reset: str = "hard"):
+        super().__init__()
+        self.decay, self.v_th, self.v_reset, self.alpha, self.reset = decay, v_th, v_reset, alpha, reset
+
+    def cfg(self, dtype: torch.dtype) -> layer.LifConfig:
+        return layer.LifConfig(self.decay, self.v_th, self.v_reset, self.alpha, self.reset, _IO[dtype], "io")
+
+    def forward(self, x: torch.Tensor) -> torch.Tensor:
+        return FusedLIF.apply(x, self.cfg(x.dtype))
+
+    def extra_repr(self) -> str:
+        return (f"decay={self.decay}, v_th={self.v_th}, v_reset={self.v_reset}, alpha={self.alpha}, "
+                f"reset={self.reset}")

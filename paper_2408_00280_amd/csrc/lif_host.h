@@ -1,0 +1,126 @@
+// Host-side planning and launching for the fused LIF library: argument checks, the lane /
+// chunk plan shared by forward and backward, and the per-translation-unit launchers.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <tuple>
+#include <utility>
+
+#include "lif_common.h"
+
+namespace snnlif {
+
+inline snn_status check_cfg(const snn_lif_cfg* c) {
+    if (c == nullptr) return SNN_E_NULL;
+    if (!(c->decay >= 0.0f && c->decay <= 1.0f)) return SNN_E_PARAM;  // also rejects NaN
+    if (!std::isfinite(c->v_th) || !std::isfinite(c->v_reset)) return SNN_E_PARAM;
+    if (!(c->alpha > 0.0f) || !std::isfinite(c->alpha)) return SNN_E_PARAM;
+    if (c->reset != SNN_RESET_HARD && c->reset != SNN_RESET_SOFT) return SNN_E_PARAM;
+    if (c->io != SNN_IO_F32 && c->io != SNN_IO_BF16) return SNN_E_PARAM;
+    if (c->spk != SNN_SPK_U8 && c->spk != SNN_SPK_BITS && c->spk != SNN_SPK_IO) return SNN_E_PARAM;
+    return SNN_OK;
+}
+
+inline snn_status check_shape(int64_t T, int64_t N) {
+    if (T < 0 || N < 0 || T > kMaxT || N > kMaxN) return SNN_E_SHAPE;
+    if (T > 0 && N > kMaxTN / T) return SNN_E_SHAPE;
+    return SNN_OK;
+}
+
+inline bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline int64_t io_bytes(const snn_lif_cfg* c) { return c->io == SNN_IO_F32 ? 4 : 2; }
+
+inline int64_t spike_row_bytes(const snn_lif_cfg* c, int64_t N) {
+    return c->spk == SNN_SPK_U8 ? N : c->spk == SNN_SPK_BITS ? 8 * ((N + 63) / 64) : N * io_bytes(c);
+}
+
+// Neurons per lane in the forward (vf) and the backward (vb), steps per chunk (K, also the
+// checkpoint interval, sized by the backward's register budget) and whether chunks are
+// double-buffered.  The same choice drives both kernels and the checkpoint layout (which
+// does not depend on the lane widths), so it depends only on (cfg, T, N).
+struct Plan {
+    int vf;
+    int vb;
+    int k;
+    bool pipe;
+    int64_t lanes;   // lanes in the forward grid
+    int64_t row_bytes;
+};
+
+// Steps per chunk: the backward keeps K membranes per neuron in VGPRs plus K rows of x and
+// dL/dy (twice the rows when double-buffered); bf16 rows take half the registers.
+constexpr int chunk_steps(int io, int v, bool pipe) {
+    return v == 4 ? (pipe && io == SNN_IO_F32 ? 8 : 16) : v == 2 ? 16 : 32;
+}
+
+// Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
+constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
+
+inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
+    Plan p;
+    p.vb = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
+    if (p.vb == 4 && N / 4 < kFillLanes) p.vb = 2;   // twice the lanes for small layers
+    p.pipe = T > chunk_steps(c->io, p.vb, false) && N / p.vb < 4 * kFillLanes;
+    p.k = chunk_steps(c->io, p.vb, p.pipe);
+    // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
+    p.vf = (c->io == SNN_IO_BF16 && p.vb == 4 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
+    p.row_bytes = spike_row_bytes(c, N);
+    const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
+    p.lanes = (covered + p.vf - 1) / p.vf;
+    return p;
+}
+
+inline int64_t saved_bytes(const Plan& p, int64_t T, int64_t N) {
+    const int64_t chunks = (T + p.k - 1) / p.k;
+    return chunks > 1 ? (chunks - 1) * N * int64_t(sizeof(float)) : 0;
+}
+
+inline LifK kernel_consts(const snn_lif_cfg* c) {
+    LifK k;
+    k.k = c->decay;
+    k.th = c->v_th;
+    k.rest = c->v_reset;
+    k.alpha = c->alpha;
+    k.c_exp = float(-double(c->alpha) * 1.4426950408889634074);  // -alpha log2(e)
+    k.kth = c->decay * c->v_th;
+    return k;
+}
+
+inline dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
+
+template <typename Tuple, size_t... I>
+void fill_argv(Tuple& t, void** argv, std::index_sequence<I...>) {
+    ((argv[I] = static_cast<void*>(&std::get<I>(t))), ...);
+}
+
+// Launch through hipLaunchKernel so the runtime's verdict is returned directly and the
+// caller's sticky error state is left alone.
+template <typename... P, typename... A>
+snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
+    static_assert(sizeof...(P) == sizeof...(A), "argument count");
+    std::tuple<P...> args(a...);
+    void* argv[sizeof...(P)];
+    fill_argv(args, argv, std::index_sequence_for<P...>{});
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(kBlock), argv, 0, stream);
+    return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
+}
+
+// Launchers, one per kernel translation unit (defined by explicit instantiation there).
+template <int IO, int SPK>
+snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
+                         void* spikes, void* saved, float* v_out, hipStream_t s);
+
+template <int IO>
+snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
+                          const void* saved, const void* gs, void* gx, hipStream_t s);
+
+snn_status gain_forward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_t F, const void* spikes,
+                              int64_t row_bytes, const float* gain, void* x_next, hipStream_t s);
+
+snn_status gain_backward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_t F, const void* gx_next,
+                               const float* gain, void* gs, hipStream_t s);
+
+}  // namespace snnlif

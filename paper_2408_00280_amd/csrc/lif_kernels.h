@@ -1,5 +1,6 @@
-// Temporally fused LIF layer for MI355X (gfx950): forward and backward kernels and the
-// C ABI declared in include/snn_lif.h.
+// Device code of the temporally fused LIF layer for MI355X (gfx950): forward and
+// backward kernels and the stacked-layer gain kernels.  Each kernel translation unit
+// includes this header and instantiates one slice of the kernel variants.
 //
 // Design (see the header for the operation itself):
 //  * Neurons are independent (Sec. 3.1), so each lane owns V consecutive neurons and walks
@@ -18,35 +19,15 @@
 //    this file is compiled with -ffp-contract=off), so results are reproducible
 //    bit for bit.  The backward uses fused multiply-adds where it wants them, explicitly.
 //  * No MFMA: the work is elementwise across neurons and a scalar recurrence in time.
+#pragma once
 #include <hip/hip_runtime.h>
 
-#include <climits>
-#include <cmath>
 #include <cstdint>
-#include <tuple>
 #include <type_traits>
-#include <utility>
 
-#include "snn_lif.h"
+#include "lif_common.h"
 
-namespace {
-
-constexpr int kBlock = 256;  // 4 wave64 per workgroup
-constexpr int kWave = 64;
-
-constexpr int64_t kMaxT = INT32_MAX;
-constexpr int64_t kMaxN = int64_t(1) << 31;
-constexpr int64_t kMaxTN = int64_t(1) << 44;
-
-// Kernel-side hyper-parameters.
-struct LifK {
-    float k;      // decay k_tau
-    float th;     // V_th
-    float rest;   // V_rest
-    float alpha;  // surrogate sharpness
-    float c_exp;  // -alpha * log2(e): e^{-alpha |u|} = 2^{c_exp |u|}
-    float kth;    // k * V_th (soft-reset backward)
-};
+namespace snnlif {
 
 // ------------------------------------------------------------------------------------
 // Streaming memory access.  Every tensor element is touched once per kernel, so loads
@@ -194,10 +175,10 @@ __device__ __forceinline__ float surrogate(const LifK& c, float u) {
 // with ordinary stores: the L2 merges the partial lines of neighbouring waves before they
 // reach HBM, and a following kernel that reads the spikes can find them in cache.
 template <int SPK, int V>
-struct SpikeOut;
+struct SpikeFmt;
 
 template <>
-struct SpikeOut<SNN_SPK_U8, 4> {
+struct SpikeFmt<SNN_SPK_U8, 4> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[4]) {
         const uint32_t w = uint32_t(y[0]) | (uint32_t(y[1]) << 8) | (uint32_t(y[2]) << 16) |
@@ -207,7 +188,7 @@ struct SpikeOut<SNN_SPK_U8, 4> {
 };
 
 template <>
-struct SpikeOut<SNN_SPK_U8, 8> {
+struct SpikeFmt<SNN_SPK_U8, 8> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[8]) {
         uint2 w;
@@ -218,7 +199,7 @@ struct SpikeOut<SNN_SPK_U8, 8> {
 };
 
 template <>
-struct SpikeOut<SNN_SPK_U8, 2> {
+struct SpikeFmt<SNN_SPK_U8, 2> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[2]) {
         if (active) *reinterpret_cast<uint16_t*>(s + t * row_bytes + n0) = (uint16_t(uint32_t(y[0]) | (uint32_t(y[1]) << 8)));
@@ -226,7 +207,7 @@ struct SpikeOut<SNN_SPK_U8, 2> {
 };
 
 template <>
-struct SpikeOut<SNN_SPK_U8, 1> {
+struct SpikeFmt<SNN_SPK_U8, 1> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[1]) {
         if (active) s[t * row_bytes + n0] = uint8_t(y[0]);
@@ -237,7 +218,7 @@ struct SpikeOut<SNN_SPK_U8, 1> {
 // moved to the even lane with a DPP quad permutation [1,0,3,2].  Every lane of the wave
 // executes this (no divergence around it).
 template <>
-struct SpikeOut<SNN_SPK_BITS, 4> {
+struct SpikeFmt<SNN_SPK_BITS, 4> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[4]) {
         const int nib = active ? (int(y[0]) | (int(y[1]) << 1) | (int(y[2]) << 2) | (int(y[3]) << 3)) : 0;
@@ -250,7 +231,7 @@ struct SpikeOut<SNN_SPK_BITS, 4> {
 // Bits, 2 neurons per lane: four lanes share a byte; two DPP quad permutations ([1,0,3,2]
 // then [2,3,0,1]) gather it in the first lane of each quad.
 template <>
-struct SpikeOut<SNN_SPK_BITS, 2> {
+struct SpikeFmt<SNN_SPK_BITS, 2> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[2]) {
         int b = active ? (int(y[0]) | (int(y[1]) << 1)) : 0;
@@ -262,7 +243,7 @@ struct SpikeOut<SNN_SPK_BITS, 2> {
 
 // Bits, 8 neurons per lane: each lane owns one byte of the row.
 template <>
-struct SpikeOut<SNN_SPK_BITS, 8> {
+struct SpikeFmt<SNN_SPK_BITS, 8> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[8]) {
         uint32_t b = 0;
@@ -274,12 +255,29 @@ struct SpikeOut<SNN_SPK_BITS, 8> {
 
 // Bits, 1 neuron per lane: one wave64 ballot is one 64-bit word of the row.
 template <>
-struct SpikeOut<SNN_SPK_BITS, 1> {
+struct SpikeFmt<SNN_SPK_BITS, 1> {
     __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
                                  const bool (&y)[1]) {
         const uint64_t word = __ballot(active && y[0]);
         if ((threadIdx.x & (kWave - 1)) == 0 && n0 < row_bytes * 8)
             *reinterpret_cast<uint64_t*>(s + t * row_bytes + (n0 >> 3)) = word;
+    }
+};
+
+// Spikes as 0/1 values in the I/O dtype ([T][N] like x): ready for a following ANN
+// operator.  Written through the streaming I/O path; rows are full cache lines.
+template <int IO, int SPK, int V>
+struct SpikeOut : SpikeFmt<SPK, V> {};
+
+template <int IO, int V>
+struct SpikeOut<IO, SNN_SPK_IO, V> {
+    __device__ static void store(uint8_t* s, int64_t row_bytes, int64_t t, int64_t n0, bool active,
+                                 const bool (&y)[V]) {
+        constexpr int64_t esize = IO == SNN_IO_F32 ? 4 : 2;
+        float f[V];
+#pragma unroll
+        for (int j = 0; j < V; ++j) f[j] = y[j] ? 1.0f : 0.0f;
+        if (active) IoVec<IO, V>::store(s, t * (row_bytes / esize) + n0, f);
     }
 };
 
@@ -358,7 +356,7 @@ __device__ __forceinline__ void forward_rows(const LifK& c, const typename IoVec
         if (FULL || i < kn) {
 #pragma unroll
             for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], on ? Io::get(xr[i], j) : 0.0f);
-            SpikeOut<SPK, V>::store(spikes, row_bytes, t0 + i, n0, on, y);
+            SpikeOut<IO, SPK, V>::store(spikes, row_bytes, t0 + i, n0, on, y);
             if (VOUT && on) store_f32<V>(v_out + (t0 + i) * N + n0, v);
         }
     }
@@ -640,21 +638,40 @@ __global__ __launch_bounds__(kBlock) void gain_forward_kernel(int64_t T, int64_t
     float gv[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
-    auto emit = [&](uint32_t w, int64_t t) {
-        float out[V];
+    if constexpr (SPK == SNN_SPK_IO) {   // spikes already 0/1 in the I/O dtype
+        using Io = IoVec<IO, V>;
+        auto emit = [&](const typename Io::raw& r, int64_t t) {
+            float out[V];
 #pragma unroll
-        for (int j = 0; j < V; ++j) out[j] = gv[j] * spike_of<SPK, V>(w, n0, j);
-        IoVec<IO, V>::store(x_next, t * N + n0, out);
-    };
-    int64_t t0 = 0;
-    for (; t0 + kGlueRows <= T; t0 += kGlueRows) {
-        uint32_t w[kGlueRows];
+            for (int j = 0; j < V; ++j) out[j] = gv[j] * Io::get(r, j);
+            Io::store(x_next, t * N + n0, out);
+        };
+        int64_t t0 = 0;
+        for (; t0 + kGlueRows <= T; t0 += kGlueRows) {
+            typename Io::raw r[kGlueRows];
 #pragma unroll
-        for (int i = 0; i < kGlueRows; ++i) w[i] = spike_word<SPK, V>(spikes, row_bytes, t0 + i, n0);
+            for (int i = 0; i < kGlueRows; ++i) r[i] = Io::load(spikes, (t0 + i) * N + n0);
 #pragma unroll
-        for (int i = 0; i < kGlueRows; ++i) emit(w[i], t0 + i);
+            for (int i = 0; i < kGlueRows; ++i) emit(r[i], t0 + i);
+        }
+        for (; t0 < T; ++t0) emit(Io::load(spikes, t0 * N + n0), t0);
+    } else {
+        auto emit = [&](uint32_t w, int64_t t) {
+            float out[V];
+#pragma unroll
+            for (int j = 0; j < V; ++j) out[j] = gv[j] * spike_of<SPK, V>(w, n0, j);
+            IoVec<IO, V>::store(x_next, t * N + n0, out);
+        };
+        int64_t t0 = 0;
+        for (; t0 + kGlueRows <= T; t0 += kGlueRows) {
+            uint32_t w[kGlueRows];
+#pragma unroll
+            for (int i = 0; i < kGlueRows; ++i) w[i] = spike_word<SPK, V>(spikes, row_bytes, t0 + i, n0);
+#pragma unroll
+            for (int i = 0; i < kGlueRows; ++i) emit(w[i], t0 + i);
+        }
+        for (; t0 < T; ++t0) emit(spike_word<SPK, V>(spikes, row_bytes, t0, n0), t0);
     }
-    for (; t0 < T; ++t0) emit(spike_word<SPK, V>(spikes, row_bytes, t0, n0), t0);
 }
 
 template <int IO, int V>
@@ -685,293 +702,4 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
     for (; t0 < T; ++t0) emit(Io::load(gx_next, t0 * N + n0), t0);
 }
 
-// ------------------------------------------------------------------------------------
-// Host side.
-
-template <typename Tuple, size_t... I>
-void fill_argv(Tuple& t, void** argv, std::index_sequence<I...>) {
-    ((argv[I] = static_cast<void*>(&std::get<I>(t))), ...);
-}
-
-// Launch through hipLaunchKernel so the runtime's verdict is returned directly and the
-// caller's sticky error state is left alone.
-template <typename... P, typename... A>
-snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
-    static_assert(sizeof...(P) == sizeof...(A), "argument count");
-    std::tuple<P...> args(a...);
-    void* argv[sizeof...(P)];
-    fill_argv(args, argv, std::index_sequence_for<P...>{});
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(kBlock), argv, 0, stream);
-    return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
-}
-
-snn_status check_cfg(const snn_lif_cfg* c) {
-    if (c == nullptr) return SNN_E_NULL;
-    if (!(c->decay >= 0.0f && c->decay <= 1.0f)) return SNN_E_PARAM;  // also rejects NaN
-    if (!std::isfinite(c->v_th) || !std::isfinite(c->v_reset)) return SNN_E_PARAM;
-    if (!(c->alpha > 0.0f) || !std::isfinite(c->alpha)) return SNN_E_PARAM;
-    if (c->reset != SNN_RESET_HARD && c->reset != SNN_RESET_SOFT) return SNN_E_PARAM;
-    if (c->io != SNN_IO_F32 && c->io != SNN_IO_BF16) return SNN_E_PARAM;
-    if (c->spk != SNN_SPK_U8 && c->spk != SNN_SPK_BITS) return SNN_E_PARAM;
-    return SNN_OK;
-}
-
-snn_status check_shape(int64_t T, int64_t N) {
-    if (T < 0 || N < 0 || T > kMaxT || N > kMaxN) return SNN_E_SHAPE;
-    if (T > 0 && N > kMaxTN / T) return SNN_E_SHAPE;
-    return SNN_OK;
-}
-
-bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-int64_t spike_row_bytes(const snn_lif_cfg* c, int64_t N) {
-    return c->spk == SNN_SPK_U8 ? N : 8 * ((N + 63) / 64);
-}
-
-// Neurons per lane in the forward (vf) and the backward (vb), steps per chunk (K, also the
-// checkpoint interval, sized by the backward's register budget) and whether chunks are
-// double-buffered.  The same choice drives both kernels and the checkpoint layout (which
-// does not depend on the lane widths), so it depends only on (cfg, T, N).
-struct Plan {
-    int vf;
-    int vb;
-    int k;
-    bool pipe;
-    int64_t lanes;   // lanes in the forward grid
-    int64_t row_bytes;
-};
-
-// Steps per chunk: the backward keeps K membranes per neuron in VGPRs plus K rows of x and
-// dL/dy (twice the rows when double-buffered); bf16 rows take half the registers.
-constexpr int chunk_steps(int io, int v, bool pipe) {
-    return v == 4 ? (pipe && io == SNN_IO_F32 ? 8 : 16) : v == 2 ? 16 : 32;
-}
-
-// Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
-constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
-
-Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
-    Plan p;
-    p.vb = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
-    if (p.vb == 4 && N / 4 < kFillLanes) p.vb = 2;   // twice the lanes for small layers
-    p.pipe = T > chunk_steps(c->io, p.vb, false) && N / p.vb < 4 * kFillLanes;
-    p.k = chunk_steps(c->io, p.vb, p.pipe);
-    // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
-    p.vf = (c->io == SNN_IO_BF16 && p.vb == 4 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
-    p.row_bytes = spike_row_bytes(c, N);
-    const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
-    p.lanes = (covered + p.vf - 1) / p.vf;
-    return p;
-}
-
-int64_t saved_bytes(const Plan& p, int64_t T, int64_t N) {
-    const int64_t chunks = (T + p.k - 1) / p.k;
-    return chunks > 1 ? (chunks - 1) * N * int64_t(sizeof(float)) : 0;
-}
-
-LifK kernel_consts(const snn_lif_cfg* c) {
-    LifK k;
-    k.k = c->decay;
-    k.th = c->v_th;
-    k.rest = c->v_reset;
-    k.alpha = c->alpha;
-    k.c_exp = float(-double(c->alpha) * 1.4426950408889634074);  // -alpha log2(e)
-    k.kth = c->decay * c->v_th;
-    return k;
-}
-
-dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
-
-template <int IO, int SPK, int RESET, int V, int K, bool PIPE>
-snn_status forward_launch_v(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, uint8_t* sp,
-                            float* sv, float* v_out, hipStream_t s) {
-    const dim3 g = grid_for(p.lanes);
-    return v_out ? launch(lif_forward_kernel<IO, SPK, RESET, V, K, true, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out)
-                 : launch(lif_forward_kernel<IO, SPK, RESET, V, K, false, PIPE>, g, s, k, T, N, x, sp, p.row_bytes, sv, v_out);
-}
-
-// (vf, vb, pipe) combinations the planner produces.
-template <int IO, int SPK, int RESET>
-snn_status forward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, void* spikes,
-                          void* saved, float* v_out, hipStream_t s) {
-    uint8_t* sp = static_cast<uint8_t*>(spikes);
-    float* sv = static_cast<float*>(saved);
-    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
-    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
-    if constexpr (IO == SNN_IO_BF16) {
-        if (p.vf == 8)
-            return p.pipe ? forward_launch_v<IO, SPK, RESET, 8, K4p, true>(p, k, T, N, x, sp, sv, v_out, s)
-                          : forward_launch_v<IO, SPK, RESET, 8, K4, false>(p, k, T, N, x, sp, sv, v_out, s);
-    }
-    switch (p.vf * 2 + int(p.pipe)) {
-        case 8: return forward_launch_v<IO, SPK, RESET, 4, K4, false>(p, k, T, N, x, sp, sv, v_out, s);
-        case 9: return forward_launch_v<IO, SPK, RESET, 4, K4p, true>(p, k, T, N, x, sp, sv, v_out, s);
-        case 4: return forward_launch_v<IO, SPK, RESET, 2, K2, false>(p, k, T, N, x, sp, sv, v_out, s);
-        case 5: return forward_launch_v<IO, SPK, RESET, 2, K2, true>(p, k, T, N, x, sp, sv, v_out, s);
-        case 2: return forward_launch_v<IO, SPK, RESET, 1, K1, false>(p, k, T, N, x, sp, sv, v_out, s);
-        default: return forward_launch_v<IO, SPK, RESET, 1, K1, true>(p, k, T, N, x, sp, sv, v_out, s);
-    }
-}
-
-template <int IO, int RESET, int V, bool PIPE>
-snn_status backward_launch_v(const LifK& k, int64_t T, int64_t N, const void* x, const float* sv, const void* gs,
-                             void* gx, hipStream_t s) {
-    constexpr int K = chunk_steps(IO, V, PIPE);
-    return launch(lif_backward_kernel<IO, RESET, V, K, PIPE>, grid_for((N + V - 1) / V), s, k, T, N, x, sv, gs, gx);
-}
-
-template <int IO, int RESET>
-snn_status backward_launch(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
-                           const void* saved, const void* gs, void* gx, hipStream_t s) {
-    const float* sv = static_cast<const float*>(saved);
-    switch (p.vb * 2 + int(p.pipe)) {
-        case 8: return backward_launch_v<IO, RESET, 4, false>(k, T, N, x, sv, gs, gx, s);
-        case 9: return backward_launch_v<IO, RESET, 4, true>(k, T, N, x, sv, gs, gx, s);
-        case 4: return backward_launch_v<IO, RESET, 2, false>(k, T, N, x, sv, gs, gx, s);
-        case 5: return backward_launch_v<IO, RESET, 2, true>(k, T, N, x, sv, gs, gx, s);
-        case 2: return backward_launch_v<IO, RESET, 1, false>(k, T, N, x, sv, gs, gx, s);
-        default: return backward_launch_v<IO, RESET, 1, true>(k, T, N, x, sv, gs, gx, s);
-    }
-}
-
-}  // namespace
-
-extern "C" {
-
-const char* snn_status_str(snn_status status) {
-    switch (status) {
-        case SNN_OK: return "ok";
-        case SNN_E_NULL: return "a required pointer is NULL";
-        case SNN_E_SHAPE: return "shape out of range";
-        case SNN_E_PARAM: return "hyper-parameter or enum out of range";
-        case SNN_E_ALIGN: return "data pointer not 16-byte aligned";
-        case SNN_E_UNSUPPORTED: return "unsupported combination";
-        case SNN_E_LAUNCH: return "kernel launch rejected by the HIP runtime";
-    }
-    return "unknown status";
-}
-
-snn_status snn_spike_row_bytes(const snn_lif_cfg* cfg, int64_t N, size_t* bytes) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if (bytes == nullptr) return SNN_E_NULL;
-    if ((st = check_shape(0, N)) != SNN_OK) return st;
-    *bytes = size_t(spike_row_bytes(cfg, N));
-    return SNN_OK;
-}
-
-snn_status snn_lif_saved_bytes(const snn_lif_cfg* cfg, int64_t T, int64_t N, size_t* bytes) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if (bytes == nullptr) return SNN_E_NULL;
-    if ((st = check_shape(T, N)) != SNN_OK) return st;
-    *bytes = (T == 0 || N == 0) ? 0 : size_t(saved_bytes(make_plan(cfg, T, N), T, N));
-    return SNN_OK;
-}
-
-snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, void* spikes,
-                           void* saved, float* v_out, void* stream) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if ((st = check_shape(T, N)) != SNN_OK) return st;
-    if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, T, N);
-    const bool need_saved = saved_bytes(p, T, N) > 0;
-    if (x == nullptr || spikes == nullptr || (need_saved && saved == nullptr)) return SNN_E_NULL;
-    if (!aligned(x) || !aligned(spikes) || (saved && !aligned(saved)) || (v_out && !aligned(v_out)))
-        return SNN_E_ALIGN;
-    const LifK k = kernel_consts(cfg);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool bits = cfg->spk == SNN_SPK_BITS, soft = cfg->reset == SNN_RESET_SOFT;
-    if (cfg->io == SNN_IO_F32) {
-        if (bits)
-            return soft ? forward_launch<SNN_IO_F32, SNN_SPK_BITS, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
-                        : forward_launch<SNN_IO_F32, SNN_SPK_BITS, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
-        return soft ? forward_launch<SNN_IO_F32, SNN_SPK_U8, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
-                    : forward_launch<SNN_IO_F32, SNN_SPK_U8, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
-    }
-    if (bits)
-        return soft ? forward_launch<SNN_IO_BF16, SNN_SPK_BITS, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
-                    : forward_launch<SNN_IO_BF16, SNN_SPK_BITS, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
-    return soft ? forward_launch<SNN_IO_BF16, SNN_SPK_U8, SNN_RESET_SOFT>(p, k, T, N, x, spikes, saved, v_out, s)
-                : forward_launch<SNN_IO_BF16, SNN_SPK_U8, SNN_RESET_HARD>(p, k, T, N, x, spikes, saved, v_out, s);
-}
-
-snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const void* saved,
-                            const void* grad_s, void* grad_x, void* stream) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if ((st = check_shape(T, N)) != SNN_OK) return st;
-    if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, T, N);
-    const bool need_saved = saved_bytes(p, T, N) > 0;
-    if (x == nullptr || grad_s == nullptr || grad_x == nullptr || (need_saved && saved == nullptr))
-        return SNN_E_NULL;
-    if (!aligned(x) || !aligned(grad_s) || !aligned(grad_x) || (saved && !aligned(saved))) return SNN_E_ALIGN;
-    const LifK k = kernel_consts(cfg);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool soft = cfg->reset == SNN_RESET_SOFT;
-    if (cfg->io == SNN_IO_F32)
-        return soft ? backward_launch<SNN_IO_F32, SNN_RESET_SOFT>(p, k, T, N, x, saved, grad_s, grad_x, s)
-                    : backward_launch<SNN_IO_F32, SNN_RESET_HARD>(p, k, T, N, x, saved, grad_s, grad_x, s);
-    return soft ? backward_launch<SNN_IO_BF16, SNN_RESET_SOFT>(p, k, T, N, x, saved, grad_s, grad_x, s)
-                : backward_launch<SNN_IO_BF16, SNN_RESET_HARD>(p, k, T, N, x, saved, grad_s, grad_x, s);
-}
-
-static snn_status check_gain_shape(int64_t T, int64_t B, int64_t F) {
-    if (T < 0 || B < 0 || F < 0) return SNN_E_SHAPE;
-    if (B > 0 && F > kMaxN / B) return SNN_E_SHAPE;
-    return check_shape(T, B * F);
-}
-
-static dim3 gain_grid(int64_t lanes) { return grid_for(lanes); }
-
-snn_status snn_gain_spikes_forward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes,
-                                   const float* gain, void* x_next, void* stream) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
-    const int64_t N = B * F;
-    if (T == 0 || N == 0) return SNN_OK;
-    if (spikes == nullptr || gain == nullptr || x_next == nullptr) return SNN_E_NULL;
-    if (!aligned(spikes) || !aligned(gain) || !aligned(x_next)) return SNN_E_ALIGN;
-    const int64_t row = spike_row_bytes(cfg, N);
-    const uint8_t* sp = static_cast<const uint8_t*>(spikes);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool v4 = N % 4 == 0;
-    const dim3 grid = gain_grid(v4 ? N / 4 : N);
-    const bool bits = cfg->spk == SNN_SPK_BITS;
-    if (cfg->io == SNN_IO_F32) {
-        if (v4)
-            return bits ? launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_BITS, 4>, grid, s, T, N, F, sp, row, gain, x_next)
-                        : launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_U8, 4>, grid, s, T, N, F, sp, row, gain, x_next);
-        return bits ? launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_BITS, 1>, grid, s, T, N, F, sp, row, gain, x_next)
-                    : launch(gain_forward_kernel<SNN_IO_F32, SNN_SPK_U8, 1>, grid, s, T, N, F, sp, row, gain, x_next);
-    }
-    if (v4)
-        return bits ? launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_BITS, 4>, grid, s, T, N, F, sp, row, gain, x_next)
-                    : launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_U8, 4>, grid, s, T, N, F, sp, row, gain, x_next);
-    return bits ? launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_BITS, 1>, grid, s, T, N, F, sp, row, gain, x_next)
-                : launch(gain_forward_kernel<SNN_IO_BF16, SNN_SPK_U8, 1>, grid, s, T, N, F, sp, row, gain, x_next);
-}
-
-snn_status snn_gain_grad_backward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* grad_x_next,
-                                  const float* gain, void* grad_s, void* stream) {
-    snn_status st = check_cfg(cfg);
-    if (st != SNN_OK) return st;
-    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
-    const int64_t N = B * F;
-    if (T == 0 || N == 0) return SNN_OK;
-    if (grad_x_next == nullptr || gain == nullptr || grad_s == nullptr) return SNN_E_NULL;
-    if (!aligned(grad_x_next) || !aligned(gain) || !aligned(grad_s)) return SNN_E_ALIGN;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool v4 = N % 4 == 0;
-    const dim3 grid = gain_grid(v4 ? N / 4 : N);
-    if (cfg->io == SNN_IO_F32)
-        return v4 ? launch(gain_backward_kernel<SNN_IO_F32, 4>, grid, s, T, N, F, grad_x_next, gain, grad_s)
-                  : launch(gain_backward_kernel<SNN_IO_F32, 1>, grid, s, T, N, F, grad_x_next, gain, grad_s);
-    return v4 ? launch(gain_backward_kernel<SNN_IO_BF16, 4>, grid, s, T, N, F, grad_x_next, gain, grad_s)
-              : launch(gain_backward_kernel<SNN_IO_BF16, 1>, grid, s, T, N, F, grad_x_next, gain, grad_s);
-}
-
-}  // extern "C"
+}  // namespace snnlif

@@ -23,7 +23,7 @@ class LifConfig:
     alpha: float = 4.0
     reset: str = "hard"   # "hard" (Eq. (1)) or "soft"
     io: str = "f32"       # dtype of x, dL/dy, dL/dx
-    spk: str = "u8"       # "u8" or "bits"
+    spk: str = "u8"       # "u8", "bits", or "io" (0/1 in the I/O dtype, shaped like x)
 
     def c(self) -> native.snn_lif_cfg:
         return native.make_cfg(self.decay, self.v_th, self.v_reset, self.alpha, self.reset, self.io, self.spk)
@@ -39,10 +39,14 @@ def _TN(x: torch.Tensor):
 
 
 def alloc_forward(cfg: LifConfig, T: int, N: int, device, v_out: bool = False):
-    """(spikes [T][row_bytes] uint8, saved uint8 bytes, v [T][N] float32 or None)."""
+    """(spikes, saved uint8 bytes, v [T][N] float32 or None).  Spikes are [T][row_bytes]
+    uint8 for "u8"/"bits" and [T][N] of the I/O dtype for "io"."""
     c = cfg.c()
     row = native.snn_spike_row_bytes(c, N)
-    spikes = torch.empty((T, row), dtype=torch.uint8, device=device)
+    if cfg.spk == "io":
+        spikes = torch.empty((T, N), dtype=cfg.dtype, device=device)
+    else:
+        spikes = torch.empty((T, row), dtype=torch.uint8, device=device)
     saved = torch.empty(native.snn_lif_saved_bytes(c, T, N), dtype=torch.uint8, device=device)
     v = torch.empty((T, N), dtype=torch.float32, device=device) if v_out else None
     return spikes, saved, v

@@ -1,7 +1,7 @@
 """Thin ctypes binding over the C ABI in include/snn_lif.h (libsnnlif.so).
 
-Argument marshalling only: every step of the LIF path runs in the HIP kernels of
-``csrc/snn_lif.hip``.  Functions keep the C names; tensor arguments may be torch
+Argument marshalling only: every step of the LIF path runs in the HIP kernels under
+``csrc/``.  Functions keep the C names; tensor arguments may be torch
 tensors (their ``data_ptr()`` is passed) or raw device addresses (int), and
 ``stream`` may be a ``torch.cuda.Stream``, a raw hipStream_t (int) or None for
 torch's current stream.  A non-OK status raises :class:`SnnError`.
@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(HERE, "libsnnlif.so")
 SNN_OK = 0
 SNN_RESET_HARD, SNN_RESET_SOFT = 0, 1
 SNN_IO_F32, SNN_IO_BF16 = 0, 1
-SNN_SPK_U8, SNN_SPK_BITS = 0, 1
+SNN_SPK_U8, SNN_SPK_BITS, SNN_SPK_IO = 0, 1, 2
 
 STATUS_NAMES = {0: "SNN_OK", -1: "SNN_E_NULL", -2: "SNN_E_SHAPE", -3: "SNN_E_PARAM",
                 -4: "SNN_E_ALIGN", -5: "SNN_E_UNSUPPORTED", -6: "SNN_E_LAUNCH"}
@@ -46,10 +46,10 @@ class snn_lif_cfg(ctypes.Structure):
 
 def make_cfg(decay: float, v_th: float, v_reset: float = 0.0, alpha: float = 4.0, reset="hard",
              io="f32", spk="u8") -> snn_lif_cfg:
-    """Build a cfg from Python values ("hard"/"soft", "f32"/"bf16", "u8"/"bits" or the ints)."""
+    """Build a cfg from Python values ("hard"/"soft", "f32"/"bf16", "u8"/"bits"/"io" or the ints)."""
     r = {"hard": SNN_RESET_HARD, "soft": SNN_RESET_SOFT}.get(reset, reset)
     d = {"f32": SNN_IO_F32, "bf16": SNN_IO_BF16}.get(io, io)
-    s = {"u8": SNN_SPK_U8, "bits": SNN_SPK_BITS}.get(spk, spk)
+    s = {"u8": SNN_SPK_U8, "bits": SNN_SPK_BITS, "io": SNN_SPK_IO}.get(spk, spk)
     return snn_lif_cfg(decay, v_th, v_reset, alpha, r, d, s)
 
 

@@ -79,7 +79,7 @@ def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None, gy_mag=Non
     p = oracle.Params.of(w.params)
     y_ref, v_ref = oracle.forward(p, x_np)
     gx_ref, bound = oracle.backward(p, v_ref, y_ref, gs_np, gy_mag)
-    y_gpu = parity.unpack_spikes(spikes.cpu().numpy(), w.N, w.spk)
+    y_gpu = parity.unpack_spikes(to_host_f32(spikes) if w.spk == "io" else spikes.cpu().numpy(), w.N, w.spk)
     v_gpu = None if v is None else v.cpu().numpy()
     g_gpu = to_host_f32(gx)
     if cols is not None:

@@ -21,7 +21,12 @@ ATOL = 1e-30
 
 
 def unpack_spikes(raw: np.ndarray, N: int, spk: str) -> np.ndarray:
-    """[T][row_bytes] uint8 in the library's format -> [T][N] uint8 (0/1); checks padding."""
+    """Spikes in the library's format -> [T][N] uint8 (0/1); checks padding and values.
+    u8/bits: [T][row_bytes] uint8; io: [T][N] float32 (bf16 already widened)."""
+    if spk == "io":
+        a = np.asarray(raw, dtype=np.float32)
+        assert a.shape[1] == N and np.all((a == 0) | (a == 1)), "io spikes must be exactly 0 or 1"
+        return a.astype(np.uint8)
     raw = np.ascontiguousarray(raw, dtype=np.uint8)
     if spk == "u8":
         assert raw.shape[1] == N

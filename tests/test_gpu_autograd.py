@@ -1,0 +1,78 @@
+"""The autograd binding (FusedLIF / LIFLayer) against the CPU oracle: spikes, and input
+gradients from torch's autograd through one layer and through two layers joined by a
+per-feature gain (a torch elementwise product standing in for an ANN operator)."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def H():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_harness
+    return gpu_harness
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("reset", ["hard", "soft"])
+def test_lif_layer_autograd(H, dtype, reset):
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import LIFLayer
+    T, shape = 21, (3, 5, 67)    # a multi-dimensional per-step shape, N = 1005 (ragged)
+    N = int(np.prod(shape))
+    p = H.W.LifParams(0.75, 1.0, reset=reset)
+    w = H.W.custom("autograd", T, N, p, io=dtype, spk="io", seed=31, x_dist=("normal", 0.5, 0.6))
+    x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+    x = H.to_dev(x_np, dtype).view(T, *shape).requires_grad_(True)
+    gs = H.to_dev(gs_np, dtype).view(T, *shape)
+    lif = LIFLayer(p.decay, p.v_th, p.v_reset, p.alpha, reset)
+    y = lif(x)
+    assert y.shape == x.shape and y.dtype == x.dtype
+    (y * gs).sum().backward()
+    torch.cuda.synchronize()
+    P = H.oracle.Params.of(p)
+    y_ref, v_ref = H.oracle.forward(P, x_np)
+    gx_ref, bound = H.oracle.backward(P, v_ref, y_ref, gs_np)
+    rep = H.parity.compare_forward(H.to_host_f32(y.detach()).reshape(T, N).astype(np.uint8), y_ref, v_ref, p.v_th)
+    rtol = H.parity.RTOL_BF16 if dtype == "bf16" else H.parity.RTOL_F32
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, N), gx_ref, bound, rtol, rep)
+    assert rep.ok(), str(rep)
+
+
+def test_two_layers_with_gain(H):
+    """LIF -> y * gain[f] -> LIF, gradients through torch autograd vs the oracle's stack."""
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import LIFLayer
+    T, B, F = 32, 8, 256
+    p = H.W.HARD_05
+    w = H.W.custom("two", T, B * F, p, seed=41, spk="io", x_dist=("normal", 0.4, 0.6))
+    x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+    gain_np = np.random.default_rng(5).uniform(0.5, 2.0, size=F).astype(np.float32)
+    x = torch.from_numpy(x_np).to(H.DEV).view(T, B, F).requires_grad_(True)
+    gain = torch.from_numpy(gain_np).to(H.DEV)
+    lif = LIFLayer(p.decay, p.v_th)
+    y2 = lif(lif(x) * gain)
+    (y2 * torch.from_numpy(gs_np).to(H.DEV).view(T, B, F)).sum().backward()
+    torch.cuda.synchronize()
+    P = H.oracle.Params.of(p)
+    xs, ys, vs = H.oracle.stack_forward(P, x_np, [gain_np], B, F)
+    gxs, gms = H.oracle.stack_backward(P, ys, vs, gs_np, [gain_np], B, F)
+    rep = H.parity.compare_forward(H.to_host_f32(y2.detach()).reshape(T, -1).astype(np.uint8), ys[1], vs[1], p.v_th)
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), gxs[0], gms[0], H.parity.RTOL_F32, rep)
+    assert rep.ok(), str(rep)
+
+
+def test_inside_sequential(H):
+    """LIFLayer composes with torch modules (the paper's nn.Sequential usage)."""
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import LIFLayer
+    torch.manual_seed(0)
+    model = torch.nn.Sequential(torch.nn.Linear(64, 128), LIFLayer(0.5, 1.0), torch.nn.Linear(128, 10)).to(H.DEV)
+    x = torch.randn(16, 4, 64, device=H.DEV)     # [T, batch, features]
+    out = model(x)
+    out.sum().backward()
+    assert out.shape == (16, 4, 10)
+    assert all(p.grad is not None and torch.isfinite(p.grad).all() for p in model.parameters())

@@ -29,7 +29,7 @@ PARAMS = {
     "k1": dict(decay=1.0, v_th=1.0),
     "k0": dict(decay=0.0, v_th=0.5),
 }
-COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits"]))
+COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits", "io"]))
 
 
 def _workload(H, T, N, pname, reset, io, spk, seed):
@@ -182,7 +182,8 @@ def test_workload_stack(H):
         assert rep.ok(), f"layer {l}: {rep}"
 
 
-@pytest.mark.parametrize("io,spk", [("f32", "u8"), ("f32", "bits"), ("bf16", "u8"), ("bf16", "bits")])
+@pytest.mark.parametrize("io,spk", [("f32", "u8"), ("f32", "bits"), ("f32", "io"), ("bf16", "u8"),
+                                    ("bf16", "bits"), ("bf16", "io")])
 @pytest.mark.parametrize("T,B,F", [(3, 2, 5), (9, 7, 100), (4, 3, 1024)])
 def test_gain_glue(H, io, spk, T, B, F):
     torch = H.torch
@@ -193,7 +194,7 @@ def test_gain_glue(H, io, spk, T, B, F):
     cfg = H.layer.LifConfig(0.5, 1.0, io=io, spk=spk)
     raw = y if spk == "u8" else np.packbits(
         np.pad(y, ((0, 0), (0, 8 * ((N + 63) // 64) * 8 - N))), axis=1, bitorder="little")
-    spikes = torch.from_numpy(np.ascontiguousarray(raw)).to(H.DEV)
+    spikes = H.to_dev(y.astype(np.float32), io) if spk == "io" else torch.from_numpy(np.ascontiguousarray(raw)).to(H.DEV)
     g = torch.from_numpy(gain).to(H.DEV)
     xn = torch.empty((T, N), dtype=cfg.dtype, device=H.DEV)
     H.native.snn_gain_spikes_forward(cfg.c(), T, B, F, spikes, g, xn)
