@@ -88,6 +88,75 @@ def cpu_baseline(w, x_np, gs_np, gains=None):
                       f"forward + backward, {dt:.2f} s"}
 
 
+def compare_serial(args):
+    """Fused vs serial (one launch per step) forward + backward of one layer over a sweep of
+    T: the shape of the paper's single-GPU time-step experiment.  One JSON line per T."""
+    import torch
+
+    from paper_2408_00280_amd import layer, native
+    from synth import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    base = W.WORKLOADS[args.workload if args.workload != "conv" else "paper_monolayer"]
+    for T in [int(t) for t in args.Ts.split(",")]:
+        w = base.with_T(T)
+        N = w.N
+        cfg = layer.LifConfig(w.params.decay, w.params.v_th, w.params.v_reset, w.params.alpha,
+                              w.params.reset, w.io, w.spk)
+        c = cfg.c()
+        x = torch.from_numpy(W.x_full(w)).to(dev)
+        gs = torch.from_numpy(W.gs_full(w)).to(dev)
+        spikes, saved, _ = layer.alloc_forward(cfg, T, N, dev)
+        sv = saved if saved.numel() else None
+        gx = torch.empty_like(gs)
+        v = torch.empty((T, N), dtype=torch.float32, device=dev)
+
+        # launches go to torch's current stream (the capture stream inside a graph capture)
+        def fused():
+            native.snn_lif_forward(c, T, N, x, spikes, sv, None)
+            native.snn_lif_backward(c, T, N, x, sv, gs, gx)
+
+        def serial():
+            for t in range(T):
+                native.snn_lif_serial_forward_step(c, N, x[t], v[t - 1] if t else None, v[t], spikes[t])
+            for t in range(T - 1, -1, -1):
+                native.snn_lif_serial_backward_step(c, N, v[t], gs[t], gx[t + 1] if t + 1 < T else None, gx[t])
+
+        def timed(fn, reps):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+
+        fused_ms = timed(fused, args.trials)
+        serial_ms = timed(serial, args.trials)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            serial()
+        graph_ms = timed(g.replay, args.trials)
+        # the graph replays must reproduce the eager serial result
+        gx_graph = gx.clone()
+        serial()
+        torch.cuda.synchronize()
+        assert torch.equal(gx_graph, gx), "graph replay differs from the eager serial run"
+        fused_bytes = (bytes_per_nts(w)["lif_forward"] + bytes_per_nts(w)["lif_backward"]) * T * N
+        print(json.dumps({"metric": "fused vs serial LIF forward+backward, ms per trial", "workload": w.description,
+                          "T": T, "N": N, "trials": args.trials, "fused_ms": fused_ms, "serial_ms": serial_ms,
+                          "serial_graph_ms": graph_ms, "speedup_vs_serial": serial_ms / fused_ms,
+                          "speedup_vs_serial_graph": graph_ms / fused_ms,
+                          "fused_hbm_fraction": fused_bytes / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}),
+              flush=True)
+        del x, gs, spikes, saved, gx, v, g
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -98,12 +167,20 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--with-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration runs)")
+    ap.add_argument("--compare-serial", action="store_true",
+                    help="fused vs per-step serial forward+backward over --Ts (one JSON line per T)")
+    ap.add_argument("--Ts", default="4,8,16,32,64,128,256")
+    ap.add_argument("--trials", type=int, default=20)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the LIF layer shards over neurons with no "
               "communication, so a multi-GPU run is not part of this benchmark", file=sys.stderr)
         sys.exit(2)
+
+    if args.compare_serial:
+        compare_serial(args)
+        return
 
     import numpy as np
     import torch

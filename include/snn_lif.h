@@ -121,6 +121,27 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, 
                                   const void *grad_x_next, const float *gain, void *grad_s,
                                   void *stream);
 
+/* Serial (per-time-step) baseline of the same layer: the "serial training" method that
+ * temporal fusion is compared against (Sec. 3.2, Fig. 3) -- one launch per time step, the
+ * membrane round-tripping through memory between steps.  Kept as an ablation baseline.
+ * Its arithmetic is the fused kernels' own, so a step-by-step run reproduces the fused
+ * forward and backward bit for bit.
+ *   forward step t:  x_t [N] (io dtype), v_prev [N] fp32 membrane after step t-1 (NULL for
+ *                    the first step: V_rest and no spike) -> v_t [N] fp32 (needed by the
+ *                    backward and the next step), spikes_t (one row in cfg->spk format).
+ *   backward step t: v_t [N] fp32, grad_s_t [N] io dtype, g_next [N] fp32 = dL/dv of step
+ *                    t+1 (NULL at the last step) -> grad_x_t [N] io dtype = dL/dv of step t,
+ *                    and the same value in fp32 into g_out [N] when g_out is not NULL (pass
+ *                    it as the next call's g_next; for fp32 I/O grad_x_t itself can be).
+ * The step pointers are rows of [T][N] tensors, so they need only their element alignment
+ * (and 8 bytes for bit-packed spike rows), not the 16 bytes the other entry points require. */
+snn_status snn_lif_serial_forward_step(const snn_lif_cfg *cfg, int64_t N, const void *x_t,
+                                       const float *v_prev, float *v_t, void *spikes_t,
+                                       void *stream);
+snn_status snn_lif_serial_backward_step(const snn_lif_cfg *cfg, int64_t N, const float *v_t,
+                                        const void *grad_s_t, const float *g_next, void *grad_x_t,
+                                        float *g_out, void *stream);
+
 /* Static text for a status code. */
 const char *snn_status_str(snn_status status);
 

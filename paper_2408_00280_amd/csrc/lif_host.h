@@ -29,7 +29,8 @@ inline snn_status check_shape(int64_t T, int64_t N) {
     return SNN_OK;
 }
 
-inline bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline bool aligned_to(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+inline bool aligned(const void* p) { return aligned_to(p, 16); }
 
 inline int64_t io_bytes(const snn_lif_cfg* c) { return c->io == SNN_IO_F32 ? 4 : 2; }
 
@@ -122,5 +123,11 @@ snn_status gain_forward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_
 
 snn_status gain_backward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_t F, const void* gx_next,
                                const float* gain, void* gs, hipStream_t s);
+
+snn_status serial_forward_entry(const snn_lif_cfg* c, const LifK& k, int64_t N, const void* x_t,
+                                const float* v_prev, float* v_t, void* spikes_t, hipStream_t s);
+
+snn_status serial_backward_entry(const snn_lif_cfg* c, const LifK& k, int64_t N, const float* v_t, const void* gs_t,
+                                 const float* g_next, void* gx_t, float* g_out, hipStream_t s);
 
 }  // namespace snnlif

@@ -703,3 +703,68 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
 }
 
 }  // namespace snnlif
+
+namespace snnlif {
+
+// ------------------------------------------------------------------------------------
+// Serial (per-time-step) baseline: the method temporal fusion replaces (Fig. 3).  One
+// launch per step; the membrane state round-trips through memory between steps.  The
+// arithmetic is the fused kernels' own (lif_step, surrogate, the Eq. (3) update), so the
+// results are identical bit for bit.
+
+// Step t: v_prev (fp32, NULL before the first step: V_rest, no spike) -> v_t, spikes_t.
+template <int IO, int SPK, int RESET, int V>
+__global__ __launch_bounds__(kBlock) void lif_serial_forward_kernel(LifK c, int64_t N, const void* __restrict__ x_t,
+                                                                    const float* __restrict__ v_prev,
+                                                                    float* __restrict__ v_t,
+                                                                    uint8_t* __restrict__ spikes_t,
+                                                                    int64_t row_bytes) {
+    using Io = IoVec<IO, V>;
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    const bool active = n0 < N;
+    float v[V];
+    bool y[V];
+    typename Io::raw xr;
+    if (active) {
+        xr = Io::load(x_t, n0);
+        if (v_prev != nullptr) load_f32<V>(v_prev + n0, v);
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        if (v_prev == nullptr || !active) v[j] = c.rest;
+        y[j] = v_prev != nullptr && active && v[j] >= c.th;
+        lif_step<RESET>(c, v[j], y[j], active ? Io::get(xr, j) : 0.0f);
+    }
+    SpikeOut<IO, SPK, V>::store(spikes_t, row_bytes, 0, n0, active, y);
+    if (active) store_f32<V>(v_t + n0, v);
+}
+
+// Step t, reverse time: v_t, dL/dy_t, g_next = dL/dv_{t+1} (fp32, NULL at the last step)
+// -> dL/dx_t (I/O dtype) and, if g_out is not NULL, dL/dv_t in fp32 for the next call.
+template <int IO, int RESET, int V>
+__global__ __launch_bounds__(kBlock) void lif_serial_backward_kernel(LifK c, int64_t N, const float* __restrict__ v_t,
+                                                                     const void* gs_t, const float* g_next,
+                                                                     void* gx_t, float* g_out) {
+    using Io = IoVec<IO, V>;
+    const int64_t n0 = (int64_t(blockIdx.x) * kBlock + threadIdx.x) * V;
+    if (n0 >= N) return;
+    float vt[V], g[V], out[V];
+    load_f32<V>(v_t + n0, vt);
+    if (g_next != nullptr) load_f32<V>(g_next + n0, g);
+    const typename Io::raw gr = Io::load(gs_t, n0);
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+        if (g_next == nullptr) g[j] = 0.0f;
+        const float d = surrogate(c, vt[j] - c.th);
+        float dv_next;
+        if (RESET == SNN_RESET_HARD)
+            dv_next = fmaf(fmaf(-c.k, vt[j], c.rest), d, vt[j] >= c.th ? 0.0f : c.k);
+        else
+            dv_next = fmaf(-c.kth, d, c.k);
+        out[j] = fmaf(Io::get(gr, j), d, dv_next * g[j]);
+    }
+    Io::store(gx_t, n0, out);
+    if (g_out != nullptr) store_f32<V>(g_out + n0, out);
+}
+
+}  // namespace snnlif

@@ -122,4 +122,34 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg* cfg, int64_t T, int64_t B, 
     return gain_backward_entry(cfg, T, N, F, grad_x_next, gain, grad_s, static_cast<hipStream_t>(stream));
 }
 
+snn_status snn_lif_serial_forward_step(const snn_lif_cfg* cfg, int64_t N, const void* x_t, const float* v_prev,
+                                       float* v_t, void* spikes_t, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_shape(1, N)) != SNN_OK) return st;
+    if (N == 0) return SNN_OK;
+    if (x_t == nullptr || v_t == nullptr || spikes_t == nullptr) return SNN_E_NULL;
+    const uintptr_t e = uintptr_t(io_bytes(cfg));
+    const uintptr_t es = cfg->spk == SNN_SPK_U8 ? 1 : cfg->spk == SNN_SPK_BITS ? 8 : e;
+    if (!aligned_to(x_t, e) || !aligned_to(v_t, 4) || !aligned_to(spikes_t, es) || (v_prev && !aligned_to(v_prev, 4)))
+        return SNN_E_ALIGN;
+    return serial_forward_entry(cfg, kernel_consts(cfg), N, x_t, v_prev, v_t, spikes_t,
+                                static_cast<hipStream_t>(stream));
+}
+
+snn_status snn_lif_serial_backward_step(const snn_lif_cfg* cfg, int64_t N, const float* v_t, const void* grad_s_t,
+                                        const float* g_next, void* grad_x_t, float* g_out, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_shape(1, N)) != SNN_OK) return st;
+    if (N == 0) return SNN_OK;
+    if (v_t == nullptr || grad_s_t == nullptr || grad_x_t == nullptr) return SNN_E_NULL;
+    const uintptr_t e = uintptr_t(io_bytes(cfg));
+    if (!aligned_to(v_t, 4) || !aligned_to(grad_s_t, e) || !aligned_to(grad_x_t, e) ||
+        (g_next && !aligned_to(g_next, 4)) || (g_out && !aligned_to(g_out, 4)))
+        return SNN_E_ALIGN;
+    return serial_backward_entry(cfg, kernel_consts(cfg), N, v_t, grad_s_t, g_next, grad_x_t, g_out,
+                                 static_cast<hipStream_t>(stream));
+}
+
 }  // extern "C"

@@ -29,7 +29,8 @@ STATUS_NAMES = {0: "SNN_OK", -1: "SNN_E_NULL", -2: "SNN_E_SHAPE", -3: "SNN_E_PAR
 
 # Every symbol the header declares; a test checks the library exports all of them.
 EXPORTS = ("snn_spike_row_bytes", "snn_lif_saved_bytes", "snn_lif_forward", "snn_lif_backward",
-           "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_status_str")
+           "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_lif_serial_forward_step",
+           "snn_lif_serial_backward_step", "snn_status_str")
 
 
 class SnnError(RuntimeError):
@@ -67,6 +68,8 @@ def _load():
         "snn_lif_backward": [C, i64, i64, vp, vp, vp, vp, vp],
         "snn_gain_spikes_forward": [C, i64, i64, i64, vp, vp, vp, vp],
         "snn_gain_grad_backward": [C, i64, i64, i64, vp, vp, vp, vp],
+        "snn_lif_serial_forward_step": [C, i64, vp, vp, vp, vp, vp],
+        "snn_lif_serial_backward_step": [C, i64, vp, vp, vp, vp, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -137,3 +140,14 @@ def snn_gain_spikes_forward(cfg, T, B, F, spikes, gain, x_next, stream=None):
 def snn_gain_grad_backward(cfg, T, B, F, grad_x_next, gain, grad_s, stream=None):
     _check("snn_gain_grad_backward", lib.snn_gain_grad_backward(
         ctypes.byref(cfg), T, B, F, _ptr(grad_x_next), _ptr(gain), _ptr(grad_s), _stream(stream)))
+
+
+def snn_lif_serial_forward_step(cfg, N, x_t, v_prev, v_t, spikes_t, stream=None):
+    _check("snn_lif_serial_forward_step", lib.snn_lif_serial_forward_step(
+        ctypes.byref(cfg), N, _ptr(x_t), _ptr(v_prev), _ptr(v_t), _ptr(spikes_t), _stream(stream)))
+
+
+def snn_lif_serial_backward_step(cfg, N, v_t, grad_s_t, g_next, grad_x_t, g_out=None, stream=None):
+    _check("snn_lif_serial_backward_step", lib.snn_lif_serial_backward_step(
+        ctypes.byref(cfg), N, _ptr(v_t), _ptr(grad_s_t), _ptr(g_next), _ptr(grad_x_t), _ptr(g_out),
+        _stream(stream)))

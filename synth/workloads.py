@@ -91,6 +91,15 @@ WORKLOADS = {
 }
 LARGE_T = (4, 16, 64, 256)
 
+# A monolayer of 1,000,000 neurons with the paper's hyper-parameters (Sec. 5.1; the
+# single-GPU time-step experiment of Sec. 5.3 uses such a layer without ANN operators).
+# The paper gives no input distribution; N(0.2, 0.2) makes about a third of the steps fire.
+WORKLOADS["paper_monolayer"] = Workload(
+    "paper_monolayer", 6, 32, (1_000_000,), ("normal", 0.2, 0.2),
+    LifParams(decay=0.2, v_th=0.3, v_reset=0.0, alpha=4.0),
+    description="monolayer of 1,000,000 LIF neurons, k_tau 0.2, V_th 0.3, V_rest 0, alpha 4, "
+                "x ~ N(0.2, 0.2), fp32, u8 spikes, hard reset")
+
 # The paper's own hyper-parameters (Sec. 5.1): V_rest = 0, k_tau = 0.2, V_th = 0.3, alpha = 4.
 PAPER_PARAMS = LifParams(decay=0.2, v_th=0.3, v_reset=0.0, alpha=4.0)
 
