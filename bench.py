@@ -9,7 +9,10 @@ dominant kernel (the backward) from HIP events recorded on the launch stream aro
 launch, and the CPU oracle's throughput on the host as a baseline.
 
     python bench.py [--steps K] [--warmup W] [--workload conv|single|long|stack|large]
-                    [--T T] [--no-cpu-baseline] [--with-copy]
+                    [--T T] [--fused-stack] [--no-cpu-baseline] [--with-copy]
+
+--fused-stack runs a stack's layers after the first fed straight from the previous
+layer's spikes through the gain (no stored input current or dL/dx between layers).
 
 Workloads whose buffers are smaller than the 256 MB Infinity Cache rotate over several
 independent buffer sets (about 1 GiB in total), one set per step, so that a step does not
@@ -37,10 +40,13 @@ ROTATE_BYTES = 1 << 30
 def bytes_per_nts(w):
     """Algorithmic HBM bytes per neuron-timestep: each I/O tensor read or written once.
     LIF forward: read x, write spikes; LIF backward: read x (recompute) and dL/dy, write
-    dL/dx; gain forward: read spikes, write x_next; gain backward: read and write."""
+    dL/dx; gain forward: read spikes, write x_next; gain backward: read and write.  The
+    gain-fed layer: forward reads the previous spikes and writes its own; backward reads
+    the previous spikes and dL/dy, writes dL/d(previous spikes)."""
     e = 4 if w.io == "f32" else 2
     s = 1.0 if w.spk == "u8" else 0.125
-    return {"lif_forward": e + s, "lif_backward": 3 * e, "gain_forward": s + e, "gain_backward": 2 * e}
+    return {"lif_forward": e + s, "lif_backward": 3 * e, "gain_forward": s + e, "gain_backward": 2 * e,
+            "lif_forward_gain": 2 * s, "lif_backward_gain": s + 2 * e}
 
 
 def source_hash() -> str:
@@ -164,6 +170,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="conv")
     ap.add_argument("--T", type=int, default=None, help="override T (large workload sweep)")
+    ap.add_argument("--fused-stack", action="store_true",
+                    help="stack: layers after the first read the previous spikes through the gain")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--with-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration runs)")
@@ -240,8 +248,28 @@ def main():
     bpn = bytes_per_nts(w)
     nts = T * N
 
+    fused = args.fused_stack and L > 1
+
+    def launches_fused(st):
+        out = [("lif_forward", bpn["lif_forward"] * nts, lambda: native.snn_lif_forward(
+            c, T, N, st["x"][0], st["spk"][0], st["saved"][0], None, s_ptr))]
+        for l in range(1, L):
+            out.append(("lif_forward_gain", bpn["lif_forward_gain"] * nts, lambda l=l: native.snn_lif_forward_gain(
+                c, T, B, F, st["spk"][l - 1], gains[l - 1], st["spk"][l], st["saved"][l], None, s_ptr)))
+        for l in range(L - 1, 0, -1):
+            gy = st["gs"] if l == L - 1 else st["g"][l + 1]
+            out.append(("lif_backward_gain", bpn["lif_backward_gain"] * nts,
+                        lambda l=l, gy=gy: native.snn_lif_backward_gain(
+                            c, T, B, F, st["spk"][l - 1], gains[l - 1], st["saved"][l], gy, st["g"][l], s_ptr)))
+        gy = st["gs"] if L == 1 else st["g"][1]
+        out.append(("lif_backward", bpn["lif_backward"] * nts, lambda: native.snn_lif_backward(
+            c, T, N, st["x"][0], st["saved"][0], gy, st["g"][0], s_ptr)))
+        return out
+
     def launches(st):
         """The kernels of one step, in order: (kernel, algorithmic bytes, call)."""
+        if fused:
+            return launches_fused(st)
         out = []
         for l in range(L):
             out.append(("lif_forward", bpn["lif_forward"] * nts, lambda l=l: native.snn_lif_forward(
@@ -301,8 +329,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
 
-    wtag = f"{w.name}_T{T}_N{N}"
-    dom = kernels["lif_backward_kernel"]
+    wtag = f"{w.name}{'fused' if fused else ''}_T{T}_N{N}"
+    # the dominant kernel: the largest share of the step's kernel time
+    dom_name = max(kernels, key=lambda k: kernels[k]["avg_launch_ms"] * kernels[k]["launches_per_step"])
+    dom = kernels[dom_name]
     for name in kernels:
         kernels[name]["traffic"] = measured_traffic(name.replace("_kernel", ""), wtag)
     out = {
@@ -321,12 +351,13 @@ def main():
         "config": {"workload": w.description, "T": T, "N": N, "layers": L, "dims": list(w.dims), "io": w.io,
                    "spikes": w.spk, "reset": w.params.reset, "decay": w.params.decay,
                    "v_th": w.params.v_th, "alpha": w.params.alpha, "buffer_sets": R,
+                   "schedule": "fused across the gain" if fused else "layer by layer",
                    "parallelism": "none (1 GPU)"},
         "hbm_fraction_step": step_bytes / (step_kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": "lif_backward_kernel", "bound": "hbm", "achieved": dom["GB/s"],
+        "roofline": {"kernel": dom_name, "bound": "hbm", "achieved": dom["GB/s"],
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": dom["GB/s"] / HBM_PEAK_GBS,
-                     "traffic": dom["traffic"], "algorithmic_bytes_per_launch": bpn["lif_backward"] * nts,
-                     "bytes_per_nts": bpn["lif_backward"], "avg_launch_ms": dom["avg_launch_ms"]},
+                     "traffic": dom["traffic"], "algorithmic_bytes_per_launch": dom["bytes_per_nts"] * nts,
+                     "bytes_per_nts": dom["bytes_per_nts"], "avg_launch_ms": dom["avg_launch_ms"]},
         "kernels": kernels,
         "kernel_source_sha256_16": source_hash(),
     }

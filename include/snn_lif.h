@@ -121,6 +121,32 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, 
                                   const void *grad_x_next, const float *gain, void *grad_s,
                                   void *stream);
 
+/* A LIF layer fused with the gain in front of it: the layer whose input current is
+ * x[t][b][f] = gain[f] * spikes_in[t][b][f], read directly from the previous layer's spikes
+ * instead of from a stored x.  Sec. 5 feeds LIF layers from an ANN operator (Listing 1's
+ * nn.Sequential); fusing that operator into the layer goes beyond the paper and is
+ * offered for the per-feature gain above only.  Same shapes as the gain functions
+ * (N = B*F, neuron (b, f) at b*F + f); everything else as snn_lif_forward / backward.
+ *   spikes_in  previous layer's spikes, in THIS cfg's spike format, which must be
+ *              SNN_SPK_U8 or SNN_SPK_BITS (SNN_E_UNSUPPORTED otherwise).
+ *   gain       device float32 [F].  The input current uses gain[f] rounded to cfg->io,
+ *              so the layer's spikes, membranes and checkpoints equal, bit for bit, those
+ *              of snn_gain_spikes_forward followed by snn_lif_forward.
+ * forward_gain: spikes, saved, v_out as in snn_lif_forward.
+ * backward_gain: spikes_in, gain, saved exactly as in the matching forward_gain; grad_s
+ *              [T][N] io: dL/dy of this layer; grad_s_in [T][N] io out: dL/d spikes_in =
+ *              gain[f] * dL/dx, formed in fp32 and rounded once to the io dtype (the
+ *              unfused pair rounds dL/dx first, so bf16 results may differ there in the
+ *              last bit).  grad_s_in may be the same buffer as grad_s; no other overlap.
+ * x is never materialised: per (t, n) the forward reads 1 B (u8) or 1/8 B (bits) of input
+ * instead of 4 B or 2 B. */
+snn_status snn_lif_forward_gain(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
+                                const void *spikes_in, const float *gain, void *spikes,
+                                void *saved, float *v_out, void *stream);
+snn_status snn_lif_backward_gain(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
+                                 const void *spikes_in, const float *gain, const void *saved,
+                                 const void *grad_s, void *grad_s_in, void *stream);
+
 /* Serial (per-time-step) baseline of the same layer: the "serial training" method that
  * temporal fusion is compared against (Sec. 3.2, Fig. 3) -- one launch per time step, the
  * membrane round-tripping through memory between steps.  Kept as an ablation baseline.

@@ -1,45 +1,67 @@
-// Backward-kernel launcher for one I/O dtype, chosen at build time by SNNLIF_IO.
+// Backward-kernel launchers for one I/O dtype, chosen at build time by SNNLIF_IO.  With
+// SNNLIF_GAIN=1 (and SNNLIF_SPK) the unit holds the backward of the layer fed by the previous
+// layer's spikes through a per-feature gain.
 #include "lif_host.h"
 #include "lif_kernels.h"
 
 #if !defined(SNNLIF_IO)
 #error "build with -DSNNLIF_IO=<snn_io>"
 #endif
+#ifndef SNNLIF_GAIN
+#define SNNLIF_GAIN 0
+#endif
 
 namespace snnlif {
-namespace {
 
-template <int IO, int RESET, int V, bool PIPE>
-snn_status backward_v(const LifK& k, int64_t T, int64_t N, const void* x, const float* sv, const void* gs, void* gx,
-                      hipStream_t s) {
-    constexpr int K = chunk_steps(IO, V, PIPE);
-    return launch(lif_backward_kernel<IO, RESET, V, K, PIPE>, grid_for((N + V - 1) / V), s, k, T, N, x, sv, gs, gx);
-}
-
-template <int IO, int RESET>
-snn_status backward_plan(const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x, const void* saved,
-                         const void* gs, void* gx, hipStream_t s) {
-    const float* sv = static_cast<const float*>(saved);
-    switch (p.vb * 2 + int(p.pipe)) {
-        case 8: return backward_v<IO, RESET, 4, false>(k, T, N, x, sv, gs, gx, s);
-        case 9: return backward_v<IO, RESET, 4, true>(k, T, N, x, sv, gs, gx, s);
-        case 4: return backward_v<IO, RESET, 2, false>(k, T, N, x, sv, gs, gx, s);
-        case 5: return backward_v<IO, RESET, 2, true>(k, T, N, x, sv, gs, gx, s);
-        case 2: return backward_v<IO, RESET, 1, false>(k, T, N, x, sv, gs, gx, s);
-        default: return backward_v<IO, RESET, 1, true>(k, T, N, x, sv, gs, gx, s);
-    }
-}
-
-}  // namespace
+#if !SNNLIF_GAIN
 
 template <int IO>
 snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
                           const void* saved, const void* gs, void* gx, hipStream_t s) {
-    return reset == SNN_RESET_SOFT ? backward_plan<IO, SNN_RESET_SOFT>(p, k, T, N, x, saved, gs, gx, s)
-                                   : backward_plan<IO, SNN_RESET_HARD>(p, k, T, N, x, saved, gs, gx, s);
+    const float* sv = static_cast<const float*>(saved);
+    auto go = [&](auto rst) {
+        return backward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
+            constexpr int R = decltype(rst)::value;
+            constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
+            constexpr bool Pc = decltype(PIPE)::value;
+            return launch(lif_backward_kernel<IO, R, Vc, Kc, Pc>, grid_for((N + Vc - 1) / Vc), s, k, T, N, x, sv,
+                          gs, gx);
+        });
+    };
+    return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});
 }
 
 template snn_status backward_entry<SNNLIF_IO>(int, const Plan&, const LifK&, int64_t, int64_t, const void*,
                                               const void*, const void*, void*, hipStream_t);
+
+#else
+
+#if !defined(SNNLIF_SPK)
+#error "build the gain unit with -DSNNLIF_SPK=<snn_spk>"
+#endif
+
+template <int IO, int SPK>
+snn_status backward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
+                               const void* spikes_in, const float* gain, const void* saved, const void* gs,
+                               void* gs_in, hipStream_t s) {
+    const uint8_t* si = static_cast<const uint8_t*>(spikes_in);
+    const float* sv = static_cast<const float*>(saved);
+    auto go = [&](auto rst) {
+        return backward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
+            constexpr int R = decltype(rst)::value;
+            constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
+            constexpr bool Pc = decltype(PIPE)::value;
+            return launch(lif_backward_gain_kernel<IO, SPK, R, Vc, Kc, Pc>, grid_for((N + Vc - 1) / Vc), s, k, T, N,
+                          F, si, gain, p.row_bytes, sv, gs, gs_in);
+        });
+    };
+    return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});
+}
+
+template snn_status backward_gain_entry<SNNLIF_IO, SNNLIF_SPK>(int, const Plan&, const LifK&, int64_t, int64_t,
+                                                               int64_t, const void*, const float*, const void*,
+                                                               const void*, void*, hipStream_t);
+
+#endif
 
 }  // namespace snnlif

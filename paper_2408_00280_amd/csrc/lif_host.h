@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdint>
 #include <tuple>
+#include <type_traits>
 #include <utility>
 
 #include "lif_common.h"
@@ -109,6 +110,44 @@ snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
     return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
 }
 
+// Calls f(V, K, PIPE) -- std::integral_constant / bool_constant tags -- with the lane width
+// and chunk length the plan chose for the forward (vf) or the backward (vb): the
+// combinations a kernel translation unit instantiates.
+template <int I>
+using IntC = std::integral_constant<int, I>;
+
+template <int IO, typename F>
+snn_status forward_variant(const Plan& p, F&& f) {
+    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
+    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
+    if constexpr (IO == SNN_IO_BF16) {
+        if (p.vf == 8)   // 8-wide lanes keep the chunk of the 4-wide backward they pair with
+            return p.pipe ? f(IntC<8>{}, IntC<K4p>{}, std::true_type{}) : f(IntC<8>{}, IntC<K4>{}, std::false_type{});
+    }
+    switch (p.vf * 2 + int(p.pipe)) {
+        case 8: return f(IntC<4>{}, IntC<K4>{}, std::false_type{});
+        case 9: return f(IntC<4>{}, IntC<K4p>{}, std::true_type{});
+        case 4: return f(IntC<2>{}, IntC<K2>{}, std::false_type{});
+        case 5: return f(IntC<2>{}, IntC<K2>{}, std::true_type{});
+        case 2: return f(IntC<1>{}, IntC<K1>{}, std::false_type{});
+        default: return f(IntC<1>{}, IntC<K1>{}, std::true_type{});
+    }
+}
+
+template <int IO, typename F>
+snn_status backward_variant(const Plan& p, F&& f) {
+    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
+    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
+    switch (p.vb * 2 + int(p.pipe)) {
+        case 8: return f(IntC<4>{}, IntC<K4>{}, std::false_type{});
+        case 9: return f(IntC<4>{}, IntC<K4p>{}, std::true_type{});
+        case 4: return f(IntC<2>{}, IntC<K2>{}, std::false_type{});
+        case 5: return f(IntC<2>{}, IntC<K2>{}, std::true_type{});
+        case 2: return f(IntC<1>{}, IntC<K1>{}, std::false_type{});
+        default: return f(IntC<1>{}, IntC<K1>{}, std::true_type{});
+    }
+}
+
 // Launchers, one per kernel translation unit (defined by explicit instantiation there).
 template <int IO, int SPK>
 snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
@@ -117,6 +156,18 @@ snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int
 template <int IO>
 snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
                           const void* saved, const void* gs, void* gx, hipStream_t s);
+
+// The layer fed by the previous layer's spikes (format SPK, u8 or bits) through a per-feature
+// gain of F features.
+template <int IO, int SPK>
+snn_status forward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
+                              const void* spikes_in, const float* gain, void* spikes, void* saved, float* v_out,
+                              hipStream_t s);
+
+template <int IO, int SPK>
+snn_status backward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
+                               const void* spikes_in, const float* gain, const void* saved, const void* gs,
+                               void* gs_in, hipStream_t s);
 
 snn_status gain_forward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_t F, const void* spikes,
                               int64_t row_bytes, const float* gain, void* x_next, hipStream_t s);

@@ -329,33 +329,73 @@ __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
 // range run a path with no per-lane guards (ALL = true), checkpoint loads are issued before
 // the row loads they precede in use, and double-buffered loops peel their first iteration
 // so that the loop body issues every load unconditionally.
-template <int IO, int V, int K, bool FULL, bool REV>
-__device__ __forceinline__ void load_rows(typename IoVec<IO, V>::raw (&buf)[K], const void* src, int64_t N,
-                                          int64_t t0, int kn, int64_t n0) {
-    using Io = IoVec<IO, V>;
+//
+// Where the input current comes from is a policy:
+//   DenseIn     -- x[T][N] in the I/O dtype (a layer fed by an ANN operator);
+//   GainSpikeIn -- x[t][b][f] = gain[f] * spikes_in[t][b][f], read straight from the previous
+//                  layer's spikes (a stack fused across its per-feature gain; the gain is
+//                  rounded to the I/O dtype first, as a stored input current would be).
+template <int IO, int V>
+struct DenseIn {
+    using raw = typename IoVec<IO, V>::raw;
+    const void* x;
+    __device__ raw load(int64_t N, int64_t t, int64_t n0) const { return IoVec<IO, V>::load(x, t * N + n0); }
+    __device__ float get(const raw& r, int j, int64_t) const { return IoVec<IO, V>::get(r, j); }
+};
+
+template <int IO, int SPK, int V>
+struct GainSpikeIn {
+    using raw = std::conditional_t<SPK == SNN_SPK_U8 && V == 8, uint64_t, uint32_t>;
+    const uint8_t* s;
+    int64_t row_bytes;
+    float gx[V];   // gain of the lane's neurons, rounded to the I/O dtype (forward input)
+    float gy[V];   // gain in fp32 (backward output)
+    __device__ void init(const float* gain, int64_t F, int64_t n0, bool active) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            gy[j] = active ? gain[(n0 + j) % F] : 0.0f;
+            gx[j] = IO == SNN_IO_BF16 ? bf16_lo(pack_bf16x2(gy[j], 0.0f)) : gy[j];
+        }
+    }
+    __device__ raw load(int64_t, int64_t t, int64_t n0) const {
+        const uint8_t* row = s + t * row_bytes;
+        if constexpr (SPK == SNN_SPK_BITS) return row[n0 >> 3];
+        else if constexpr (V == 8) return *reinterpret_cast<const uint64_t*>(row + n0);
+        else if constexpr (V == 4) return *reinterpret_cast<const uint32_t*>(row + n0);
+        else if constexpr (V == 2) return *reinterpret_cast<const uint16_t*>(row + n0);
+        else return row[n0];
+    }
+    __device__ float get(const raw& r, int j, int64_t n0) const {
+        const uint32_t bit = SPK == SNN_SPK_BITS ? uint32_t(r >> ((n0 + j) & 7)) & 1u : uint32_t(r >> (8 * j)) & 1u;
+        return gx[j] * float(bit);
+    }
+};
+
+template <typename In, int K, bool FULL, bool REV>
+__device__ __forceinline__ void load_rows(const In& in, typename In::raw (&buf)[K], int64_t N, int64_t t0, int kn,
+                                          int64_t n0) {
     if constexpr (REV) {
 #pragma unroll
         for (int i = K - 1; i >= 0; --i)
-            if (FULL || i < kn) buf[i] = Io::load(src, (t0 + i) * N + n0);
+            if (FULL || i < kn) buf[i] = in.load(N, t0 + i, n0);
     } else {
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            if (FULL || i < kn) buf[i] = Io::load(src, (t0 + i) * N + n0);
+            if (FULL || i < kn) buf[i] = in.load(N, t0 + i, n0);
     }
 }
 
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL, bool ALL>
-__device__ __forceinline__ void forward_rows(const LifK& c, const typename IoVec<IO, V>::raw (&xr)[K], int64_t N,
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool FULL, bool ALL, typename In>
+__device__ __forceinline__ void forward_rows(const LifK& c, const In& in, const typename In::raw (&xr)[K], int64_t N,
                                              int64_t t0, int kn, int64_t n0, bool active,
                                              uint8_t* __restrict__ spikes, int64_t row_bytes,
                                              float* __restrict__ v_out, float (&v)[V], bool (&y)[V]) {
-    using Io = IoVec<IO, V>;
     const bool on = ALL || active;
 #pragma unroll
     for (int i = 0; i < K; ++i) {
         if (FULL || i < kn) {
 #pragma unroll
-            for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], on ? Io::get(xr[i], j) : 0.0f);
+            for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[j], y[j], on ? in.get(xr[i], j, n0) : 0.0f);
             SpikeOut<IO, SPK, V>::store(spikes, row_bytes, t0 + i, n0, on, y);
             if (VOUT && on) store_f32<V>(v_out + (t0 + i) * N + n0, v);
         }
@@ -367,12 +407,11 @@ __device__ __forceinline__ void forward_rows(const LifK& c, const typename IoVec
 // checkpointed to saved[chunk][N].  PIPE: double-buffered chunks -- the next chunk's rows
 // are in flight while the current chunk is computed (for layers with few lanes, where
 // occupancy alone cannot hide the memory latency).
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE, bool ALL>
-__device__ __forceinline__ void forward_lanes(const LifK& c, int64_t T, int64_t N, int64_t n0,
-                                              const void* __restrict__ x, uint8_t* __restrict__ spikes,
-                                              int64_t row_bytes, float* __restrict__ saved,
-                                              float* __restrict__ v_out) {
-    using raw = typename IoVec<IO, V>::raw;
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE, bool ALL, typename In>
+__device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
+                                              uint8_t* __restrict__ spikes, int64_t row_bytes,
+                                              float* __restrict__ saved, float* __restrict__ v_out) {
+    using raw = typename In::raw;
     const bool active = ALL || n0 < N;
     float v[V];
     bool y[V];
@@ -389,12 +428,12 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, int64_t T, int64_t 
     // and back-edge and make the compiler's waits conservative.
     auto load = [&](raw (&buf)[K], int64_t ch) {
         __builtin_amdgcn_sched_barrier(0);
-        if (ALL || active) load_rows<IO, V, K, true, false>(buf, x, N, ch * K, K, n0);
+        if (ALL || active) load_rows<In, K, true, false>(in, buf, N, ch * K, K, n0);
         __builtin_amdgcn_sched_barrier(0);
     };
-    // CKPT: 1 = this chunk is never the last (checkpoint unconditionally), 0 = test at run time
+    // ckpt: true_type = this chunk is never the last (checkpoint unconditionally)
     auto step = [&](const raw (&buf)[K], int64_t ch, auto ckpt) {
-        forward_rows<IO, SPK, RESET, V, K, VOUT, true, ALL>(c, buf, N, ch * K, K, n0, active, spikes, row_bytes,
+        forward_rows<IO, SPK, RESET, V, K, VOUT, true, ALL>(c, in, buf, N, ch * K, K, n0, active, spikes, row_bytes,
                                                             v_out, v, y);
         if ((decltype(ckpt)::value || ch < last) && (ALL || active)) store_f32<V>(saved + ch * N + n0, v);
     };
@@ -434,8 +473,8 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, int64_t T, int64_t 
         }
     }
     if (k_tail) {
-        if (ALL || active) load_rows<IO, V, K, false, false>(a, x, N, n_full * K, k_tail, n0);
-        forward_rows<IO, SPK, RESET, V, K, VOUT, false, ALL>(c, a, N, n_full * K, k_tail, n0, active, spikes,
+        if (ALL || active) load_rows<In, K, false, false>(in, a, N, n_full * K, k_tail, n0);
+        forward_rows<IO, SPK, RESET, V, K, VOUT, false, ALL>(c, in, a, N, n_full * K, k_tail, n0, active, spikes,
                                                              row_bytes, v_out, v, y);
     }
 }
@@ -451,16 +490,41 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
                                                              float* __restrict__ v_out) {
     const int64_t first = xcd_contiguous_block() * kBlock * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    const DenseIn<IO, V> in{x};
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, T, N, n0, x, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
     else
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, T, N, n0, x, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+}
+
+// The same forward with the input current read from the previous layer's spikes through
+// the per-feature gain (neuron n has feature n % F).  Spikes in and out share the format.
+template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
+__global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_t T, int64_t N, int64_t F,
+                                                                  const uint8_t* __restrict__ spikes_in,
+                                                                  const float* __restrict__ gain,
+                                                                  uint8_t* __restrict__ spikes,
+                                                                  int64_t row_bytes,
+                                                                  float* __restrict__ saved,
+                                                                  float* __restrict__ v_out) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    GainSpikeIn<IO, SPK, V> in;
+    in.s = spikes_in;
+    in.row_bytes = row_bytes;
+    in.init(gain, F, n0, n0 < N);
+    if (first + kBlock * V <= N)
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+    else
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
 }
 
 // Backward of one chunk.  v/y enter as the state before the chunk's first step; g enters
 // as dL/dv of the step after the chunk and leaves as dL/dv of the chunk's first step.
-template <int IO, int RESET, int V, int K, bool FULL>
-__device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVec<IO, V>::raw (&xr)[K],
+// GAIN: the stored gradient is the fused stack's dL/dy of the previous layer,
+// gain[f] * dL/dx, instead of dL/dx.
+template <int IO, int RESET, int V, int K, bool FULL, bool GAIN, typename In>
+__device__ __forceinline__ void backward_rows(const LifK& c, const In& in, const typename In::raw (&xr)[K],
                                               const typename IoVec<IO, V>::raw (&gr)[K], int64_t N, int64_t t0,
                                               int kn, int64_t n0, void* gx, float (&v)[V], bool (&y)[V],
                                               float (&g)[V]) {
@@ -472,7 +536,7 @@ __device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVe
         if (FULL || i < kn) {
 #pragma unroll
             for (int j = 0; j < V; ++j) {
-                lif_step<RESET>(c, v[j], y[j], Io::get(xr[i], j));
+                lif_step<RESET>(c, v[j], y[j], in.get(xr[i], j, n0));
                 vs[i][j] = v[j];
             }
         }
@@ -492,7 +556,8 @@ __device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVe
                 else                          // k (1 - V_th delta^t)
                     dv_next = fmaf(-c.kth, d, c.k);
                 g[j] = fmaf(Io::get(gr[i], j), d, dv_next * g[j]);
-                out[j] = g[j];
+                if constexpr (GAIN) out[j] = in.gy[j] * g[j];
+                else out[j] = g[j];
             }
             Io::store(gx, (t0 + i) * N + n0, out);
         }
@@ -501,17 +566,17 @@ __device__ __forceinline__ void backward_rows(const LifK& c, const typename IoVe
 
 // Everything the backward of chunk ch reads: the state entering it (loaded first), its
 // input rows, and its dL/dy rows (issued last-first, the order the reverse pass uses them).
-template <int IO, int V, int K>
+template <int IO, int V, int K, typename In>
 struct BwdChunk {
-    typename IoVec<IO, V>::raw x[K];
+    typename In::raw x[K];
     typename IoVec<IO, V>::raw gs[K];
     float v[V];
 };
 
 // ALWAYS: the layer has a checkpoint row, so the state is loaded unconditionally (chunk 0
 // reads row 0 and then takes V_rest instead), keeping the caller's loop free of branches.
-template <int IO, int V, int K, bool FULL, bool ALWAYS>
-__device__ __forceinline__ void backward_load(BwdChunk<IO, V, K>& b, const LifK& c, const void* __restrict__ x,
+template <int IO, int V, int K, bool FULL, bool ALWAYS, typename In>
+__device__ __forceinline__ void backward_load(BwdChunk<IO, V, K, In>& b, const LifK& c, const In& in,
                                               const float* __restrict__ saved, const void* gs, int64_t N,
                                               int64_t ch, int kn, int64_t n0) {
     if (ALWAYS) {
@@ -522,13 +587,13 @@ __device__ __forceinline__ void backward_load(BwdChunk<IO, V, K>& b, const LifK&
     } else {
         load_f32<V>(saved + (ch - 1) * N + n0, b.v);
     }
-    load_rows<IO, V, K, FULL, false>(b.x, x, N, ch * K, kn, n0);
-    load_rows<IO, V, K, FULL, true>(b.gs, gs, N, ch * K, kn, n0);
+    load_rows<In, K, FULL, false>(in, b.x, N, ch * K, kn, n0);
+    load_rows<DenseIn<IO, V>, K, FULL, true>(DenseIn<IO, V>{gs}, b.gs, N, ch * K, kn, n0);
 }
 
-template <int IO, int RESET, int V, int K, bool FULL>
-__device__ __forceinline__ void backward_chunk(const LifK& c, const BwdChunk<IO, V, K>& b, int64_t N, int64_t ch,
-                                               int kn, int64_t n0, void* gx, float (&g)[V]) {
+template <int IO, int RESET, int V, int K, bool FULL, bool GAIN, typename In>
+__device__ __forceinline__ void backward_chunk(const LifK& c, const In& in, const BwdChunk<IO, V, K, In>& b,
+                                               int64_t N, int64_t ch, int kn, int64_t n0, void* gx, float (&g)[V]) {
     float v[V];
     bool y[V];
 #pragma unroll
@@ -536,31 +601,31 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, const BwdChunk<IO,
         v[j] = ch > 0 ? b.v[j] : c.rest;
         y[j] = ch > 0 && b.v[j] >= c.th;  // a checkpoint is a post-step membrane; step 0 has y = 0
     }
-    backward_rows<IO, RESET, V, K, FULL>(c, b.x, b.gs, N, ch * K, kn, n0, gx, v, y, g);
+    backward_rows<IO, RESET, V, K, FULL, GAIN>(c, in, b.x, b.gs, N, ch * K, kn, n0, gx, v, y, g);
 }
 
 // Chunks are processed last-first: the short tail chunk (if any), then the full chunks.
-template <int IO, int RESET, int V, int K, bool PIPE>
-__device__ __forceinline__ void backward_lanes(const LifK& c, int64_t T, int64_t N, int64_t n0,
-                                               const void* __restrict__ x, const float* __restrict__ saved,
-                                               const void* gs, void* gx) {
+template <int IO, int RESET, int V, int K, bool PIPE, bool GAIN, typename In>
+__device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
+                                               const float* __restrict__ saved, const void* gs, void* gx) {
+    using Chunk = BwdChunk<IO, V, K, In>;
     float g[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
     const int64_t n_full = T / K;
     const int k_tail = int(T % K);
-    BwdChunk<IO, V, K> a;
+    Chunk a;
     if (k_tail) {
-        backward_load<IO, V, K, false, false>(a, c, x, saved, gs, N, n_full, k_tail, n0);
-        backward_chunk<IO, RESET, V, K, false>(c, a, N, n_full, k_tail, n0, gx, g);
+        backward_load<IO, V, K, false, false>(a, c, in, saved, gs, N, n_full, k_tail, n0);
+        backward_chunk<IO, RESET, V, K, false, GAIN>(c, in, a, N, n_full, k_tail, n0, gx, g);
     }
-    auto load = [&](BwdChunk<IO, V, K>& buf, int64_t ch) {
+    auto load = [&](Chunk& buf, int64_t ch) {
         __builtin_amdgcn_sched_barrier(0);
-        backward_load<IO, V, K, true, PIPE>(buf, c, x, saved, gs, N, ch, K, n0);
+        backward_load<IO, V, K, true, PIPE>(buf, c, in, saved, gs, N, ch, K, n0);
         __builtin_amdgcn_sched_barrier(0);
     };
-    auto step = [&](const BwdChunk<IO, V, K>& buf, int64_t ch) {
-        backward_chunk<IO, RESET, V, K, true>(c, buf, N, ch, K, n0, gx, g);
+    auto step = [&](const Chunk& buf, int64_t ch) {
+        backward_chunk<IO, RESET, V, K, true, GAIN>(c, in, buf, N, ch, K, n0, gx, g);
     };
     if constexpr (!PIPE) {
         for (int64_t ch = n_full - 1; ch >= 0; --ch) {
@@ -568,7 +633,7 @@ __device__ __forceinline__ void backward_lanes(const LifK& c, int64_t T, int64_t
             step(a, ch);
         }
     } else if (n_full > 0) {
-        BwdChunk<IO, V, K> b;
+        Chunk b;
         load(a, n_full - 1);
         if (n_full == 1) {
             step(a, 0);
@@ -602,7 +667,26 @@ __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T,
     const int64_t first = xcd_contiguous_block() * kBlock * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
     if (first + kBlock * V > N && n0 >= N) return;
-    backward_lanes<IO, RESET, V, K, PIPE>(c, T, N, n0, x, saved, gs, gx);
+    backward_lanes<IO, RESET, V, K, PIPE, false>(c, DenseIn<IO, V>{x}, T, N, n0, saved, gs, gx);
+}
+
+// Backward of the gain-fed layer: recomputes from the previous layer's spikes and writes
+// gain[f] * dL/dx, the gradient with respect to those spikes.
+template <int IO, int SPK, int RESET, int V, int K, bool PIPE>
+__global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64_t T, int64_t N, int64_t F,
+                                                                   const uint8_t* __restrict__ spikes_in,
+                                                                   const float* __restrict__ gain,
+                                                                   int64_t row_bytes,
+                                                                   const float* __restrict__ saved,
+                                                                   const void* gs, void* gs_in) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    if (first + kBlock * V > N && n0 >= N) return;
+    GainSpikeIn<IO, SPK, V> in;
+    in.s = spikes_in;
+    in.row_bytes = row_bytes;
+    in.init(gain, F, n0, true);
+    backward_lanes<IO, RESET, V, K, PIPE, true>(c, in, T, N, n0, saved, gs, gs_in);
 }
 
 // ------------------------------------------------------------------------------------

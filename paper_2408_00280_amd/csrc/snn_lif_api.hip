@@ -122,6 +122,64 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg* cfg, int64_t T, int64_t B, 
     return gain_backward_entry(cfg, T, N, F, grad_x_next, gain, grad_s, static_cast<hipStream_t>(stream));
 }
 
+snn_status snn_lif_forward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes_in,
+                                const float* gain, void* spikes, void* saved, float* v_out, void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    if (cfg->spk != SNN_SPK_U8 && cfg->spk != SNN_SPK_BITS) return SNN_E_UNSUPPORTED;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    const Plan p = make_plan(cfg, T, N);
+    const bool need_saved = saved_bytes(p, T, N) > 0;
+    if (spikes_in == nullptr || gain == nullptr || spikes == nullptr || (need_saved && saved == nullptr))
+        return SNN_E_NULL;
+    if (!aligned(spikes_in) || !aligned(gain) || !aligned(spikes) || (saved && !aligned(saved)) ||
+        (v_out && !aligned(v_out)))
+        return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* sv = need_saved ? saved : nullptr;
+    const int r = cfg->reset;
+    if (cfg->io == SNN_IO_F32)
+        return cfg->spk == SNN_SPK_U8
+                   ? forward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s)
+                   : forward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+    return cfg->spk == SNN_SPK_U8
+               ? forward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s)
+               : forward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+}
+
+snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes_in,
+                                 const float* gain, const void* saved, const void* grad_s, void* grad_s_in,
+                                 void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    if (cfg->spk != SNN_SPK_U8 && cfg->spk != SNN_SPK_BITS) return SNN_E_UNSUPPORTED;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    const Plan p = make_plan(cfg, T, N);
+    const bool need_saved = saved_bytes(p, T, N) > 0;
+    if (spikes_in == nullptr || gain == nullptr || grad_s == nullptr || grad_s_in == nullptr ||
+        (need_saved && saved == nullptr))
+        return SNN_E_NULL;
+    if (!aligned(spikes_in) || !aligned(gain) || !aligned(grad_s) || !aligned(grad_s_in) ||
+        (saved && !aligned(saved)))
+        return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const void* sv = need_saved ? saved : nullptr;
+    const int r = cfg->reset;
+    if (cfg->io == SNN_IO_F32)
+        return cfg->spk == SNN_SPK_U8
+                   ? backward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s)
+                   : backward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+    return cfg->spk == SNN_SPK_U8
+               ? backward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s)
+               : backward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+}
+
 snn_status snn_lif_serial_forward_step(const snn_lif_cfg* cfg, int64_t N, const void* x_t, const float* v_prev,
                                        float* v_t, void* spikes_t, void* stream) {
     snn_status st = check_cfg(cfg);

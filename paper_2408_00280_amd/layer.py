@@ -70,3 +70,29 @@ def backward(cfg: LifConfig, x: torch.Tensor, saved: torch.Tensor, grad_s: torch
         grad_x = torch.empty_like(grad_s)
     native.snn_lif_backward(cfg.c(), T, N, x, saved if saved.numel() else None, grad_s, grad_x, stream)
     return grad_x
+
+
+def forward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, B: int, F: int, *,
+                 v_out: bool = False, out=None, stream=None):
+    """Forward of the layer fed gain[f] * spikes_in (the previous layer's spikes, this cfg's
+    u8/bits format, [T][row_bytes]).  Returns (spikes, saved, v_or_None)."""
+    T = spikes_in.shape[0]
+    N = B * F
+    spikes, saved, v = out if out is not None else alloc_forward(cfg, T, N, spikes_in.device, v_out)
+    native.snn_lif_forward_gain(cfg.c(), T, B, F, spikes_in, gain, spikes, saved if saved.numel() else None, v,
+                                stream)
+    return spikes, saved, v
+
+
+def backward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, saved: torch.Tensor,
+                  grad_s: torch.Tensor, B: int, F: int, *, grad_s_in: torch.Tensor | None = None,
+                  stream=None) -> torch.Tensor:
+    """Backward of forward_gain; returns dL/d spikes_in = gain[f] * dL/dx, [T][N] in cfg's I/O
+    dtype (in place if grad_s_in is grad_s)."""
+    T = spikes_in.shape[0]
+    assert grad_s.dtype == cfg.dtype and tuple(grad_s.shape) == (T, B * F) and grad_s.is_contiguous()
+    if grad_s_in is None:
+        grad_s_in = torch.empty_like(grad_s)
+    native.snn_lif_backward_gain(cfg.c(), T, B, F, spikes_in, gain, saved if saved.numel() else None, grad_s,
+                                 grad_s_in, stream)
+    return grad_s_in

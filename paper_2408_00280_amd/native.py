@@ -29,7 +29,8 @@ STATUS_NAMES = {0: "SNN_OK", -1: "SNN_E_NULL", -2: "SNN_E_SHAPE", -3: "SNN_E_PAR
 
 # Every symbol the header declares; a test checks the library exports all of them.
 EXPORTS = ("snn_spike_row_bytes", "snn_lif_saved_bytes", "snn_lif_forward", "snn_lif_backward",
-           "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_lif_serial_forward_step",
+           "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_lif_forward_gain",
+           "snn_lif_backward_gain", "snn_lif_serial_forward_step",
            "snn_lif_serial_backward_step", "snn_status_str")
 
 
@@ -68,6 +69,8 @@ def _load():
         "snn_lif_backward": [C, i64, i64, vp, vp, vp, vp, vp],
         "snn_gain_spikes_forward": [C, i64, i64, i64, vp, vp, vp, vp],
         "snn_gain_grad_backward": [C, i64, i64, i64, vp, vp, vp, vp],
+        "snn_lif_forward_gain": [C, i64, i64, i64, vp, vp, vp, vp, vp, vp],
+        "snn_lif_backward_gain": [C, i64, i64, i64, vp, vp, vp, vp, vp, vp],
         "snn_lif_serial_forward_step": [C, i64, vp, vp, vp, vp, vp],
         "snn_lif_serial_backward_step": [C, i64, vp, vp, vp, vp, vp, vp],
     }
@@ -140,6 +143,18 @@ def snn_gain_spikes_forward(cfg, T, B, F, spikes, gain, x_next, stream=None):
 def snn_gain_grad_backward(cfg, T, B, F, grad_x_next, gain, grad_s, stream=None):
     _check("snn_gain_grad_backward", lib.snn_gain_grad_backward(
         ctypes.byref(cfg), T, B, F, _ptr(grad_x_next), _ptr(gain), _ptr(grad_s), _stream(stream)))
+
+
+def snn_lif_forward_gain(cfg, T, B, F, spikes_in, gain, spikes, saved, v_out=None, stream=None):
+    _check("snn_lif_forward_gain", lib.snn_lif_forward_gain(
+        ctypes.byref(cfg), T, B, F, _ptr(spikes_in), _ptr(gain), _ptr(spikes), _ptr(saved), _ptr(v_out),
+        _stream(stream)))
+
+
+def snn_lif_backward_gain(cfg, T, B, F, spikes_in, gain, saved, grad_s, grad_s_in, stream=None):
+    _check("snn_lif_backward_gain", lib.snn_lif_backward_gain(
+        ctypes.byref(cfg), T, B, F, _ptr(spikes_in), _ptr(gain), _ptr(saved), _ptr(grad_s), _ptr(grad_s_in),
+        _stream(stream)))
 
 
 def snn_lif_serial_forward_step(cfg, N, x_t, v_prev, v_t, spikes_t, stream=None):

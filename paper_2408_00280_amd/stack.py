@@ -2,6 +2,14 @@
 the ANN operator between spiking layers), run layer by layer in temporal-major order:
 each layer's fused kernel covers all T steps before the next layer starts (Sec. 3.2).
 
+Two schedules:
+  * unfused -- gain kernels between the layers materialise every layer's input current
+    x and, in the backward, every layer's dL/dx;
+  * fused   -- layers after the first read the previous layer's spikes and the gain
+    directly (snn_lif_forward_gain), and their backward emits dL/d(previous spikes)
+    (snn_lif_backward_gain); no x or dL/dx beyond the first layer's is stored.
+Both give the same spikes, membranes and checkpoints bit for bit.
+
 Torch allocates; every step runs in the HIP kernels behind the C ABI.
 """
 from __future__ import annotations
@@ -15,21 +23,26 @@ from . import layer, native
 
 @dataclass
 class LayerState:
-    x: torch.Tensor          # this layer's input current [T][N] (kept for the backward)
+    x: torch.Tensor | None   # this layer's input current [T][N] (None when fed through the gain)
     spikes: torch.Tensor     # [T][row_bytes]
     saved: torch.Tensor      # checkpoints
     v: torch.Tensor | None   # optional membrane output
 
 
 def forward(cfg: layer.LifConfig, x1: torch.Tensor, gains: list[torch.Tensor], B: int, F: int, *,
-            v_out: bool = False, stream=None) -> list[LayerState]:
+            v_out: bool = False, fused: bool = False, stream=None) -> list[LayerState]:
     T = x1.shape[0]
     states = []
     x = x1
     for l in range(len(gains) + 1):
+        if l > 0 and fused:
+            spikes, saved, v = layer.forward_gain(cfg, states[-1].spikes, gains[l - 1], B, F, v_out=v_out,
+                                                  stream=stream)
+            states.append(LayerState(None, spikes, saved, v))
+            continue
         spikes, saved, v = layer.forward(cfg, x, v_out=v_out, stream=stream)
         states.append(LayerState(x, spikes, saved, v))
-        if l < len(gains):
+        if l < len(gains) and not fused:
             x_next = torch.empty_like(x1)
             native.snn_gain_spikes_forward(cfg.c(), T, B, F, spikes, gains[l], x_next, stream)
             x = x_next
@@ -38,9 +51,19 @@ def forward(cfg: layer.LifConfig, x1: torch.Tensor, gains: list[torch.Tensor], B
 
 def backward(cfg: layer.LifConfig, states: list[LayerState], grad_s_last: torch.Tensor,
              gains: list[torch.Tensor], B: int, F: int, *, stream=None) -> list[torch.Tensor]:
-    """dL/dx of every layer, first layer first.  Buffers are reused in place where safe."""
+    """Gradients of the stack, first layer first.  Unfused states (every x kept): dL/dx of
+    every layer.  Fused states: dL/dx1 of the first layer, then dL/dy of layers 0 .. L-2
+    (the gradient each gain-fed layer passes to the spikes that feed it)."""
     T = grad_s_last.shape[0]
     L = len(states)
+    if L > 1 and states[1].x is None:
+        gys = [None] * (L - 1)
+        gy = grad_s_last
+        for l in range(L - 1, 0, -1):
+            st = states[l]
+            gy = layer.backward_gain(cfg, states[l - 1].spikes, gains[l - 1], st.saved, gy, B, F, stream=stream)
+            gys[l - 1] = gy
+        return [layer.backward(cfg, states[0].x, states[0].saved, gy, stream=stream)] + gys
     grads = [None] * L
     gy = grad_s_last
     for l in range(L - 1, -1, -1):
