@@ -72,26 +72,64 @@ def measured_traffic(kernel_tag: str, workload_tag: str):
     return float(m_val.group(1))
 
 
-def cpu_baseline(w, x_np, gs_np, gains=None):
-    """The CPU oracle, single-threaded, forward + backward on the given inputs."""
+def _oracle_pass(p, x_np, gs_np, gains, F):
+    """Forward + backward of the whole step through the CPU oracle."""
     import oracle
-    p = oracle.Params.of(w.params)
-    t0 = time.perf_counter()
     if gains is None:
         y, v = oracle.forward(p, x_np)
         oracle.backward(p, v, y, gs_np)
-        layers = 1
     else:
-        B = x_np.shape[1] // w.F
-        _, ys, vs = oracle.stack_forward(p, x_np, gains, B, w.F)
-        oracle.stack_backward(p, ys, vs, gs_np, gains, B, w.F)
-        layers = len(gains) + 1
-    dt = time.perf_counter() - t0
-    nts = layers * x_np.shape[0] * x_np.shape[1]
-    return {"value": nts / dt, "unit": "neuron-timesteps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{layers} layer(s) x {x_np.shape[0]} steps x {x_np.shape[1]} neurons "
-                      f"({nts} nts, {'the whole workload' if x_np.shape[1] == w.N else 'the first neurons'}), "
-                      f"forward + backward, {dt:.2f} s"}
+        B = x_np.shape[1] // F
+        _, ys, vs = oracle.stack_forward(p, x_np, gains, B, F)
+        oracle.stack_backward(p, ys, vs, gs_np, gains, B, F)
+
+
+def host_threads() -> int:
+    """Host cores this process may use (the affinity mask, capped by OMP_NUM_THREADS if set)."""
+    n = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS")
+    return max(1, min(n, int(cap))) if cap and cap.isdigit() else n
+
+
+def _repeat(fn, min_s: float = 3.0):
+    """Run fn until at least min_s seconds have passed; (seconds per run, runs)."""
+    runs, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        runs += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s:
+            return dt / runs, runs
+
+
+def cpu_baseline(w, x_np, gs_np, gains=None):
+    """The CPU oracle on the host: one thread over the sample, then the same oracle
+    functions on disjoint neuron slices, one thread per core (the slicing is harness code;
+    the oracle releases the interpreter lock inside its C calls)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+    p = oracle.Params.of(w.params)
+    layers = 1 if gains is None else len(gains) + 1
+    T, n = x_np.shape
+    nts = layers * T * n
+    dt1, runs1 = _repeat(lambda: _oracle_pass(p, x_np, gs_np, gains, w.F))
+
+    cores = host_threads()
+    unit = w.F if gains is not None else 1          # stack slices keep whole feature rows
+    groups = n // unit
+    bounds = [unit * (groups * i // cores) for i in range(cores + 1)]
+    parts = [(np.ascontiguousarray(x_np[:, a:b]), np.ascontiguousarray(gs_np[:, a:b]))
+             for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
+    with ThreadPoolExecutor(max_workers=len(parts)) as pool:
+        dtn, runsn = _repeat(lambda: list(pool.map(lambda xg: _oracle_pass(p, xg[0], xg[1], gains, w.F), parts)))
+    what = "the whole workload" if n == w.N else f"the first {n} neurons of {w.N}"
+    return {"value": nts / dtn, "unit": "neuron-timesteps/s", "cores": len(parts), "kind": "oracle",
+            "sample": f"{layers} layer(s) x {T} steps x {n} neurons ({nts} nts, {what}), forward + backward, "
+                      f"{len(parts)} threads on disjoint neuron slices, {runsn} run(s) of {dtn:.3f} s",
+            "single_thread": {"value": nts / dt1, "cores": 1, "seconds_per_run": dt1, "runs": runs1}}
 
 
 def compare_serial(args):
@@ -163,6 +201,52 @@ def compare_serial(args):
         torch.cuda.empty_cache()
 
 
+def graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev):
+    """`trials` independent forward+backward pairs of one layer, captured into one HIP graph
+    and replayed (the paper measures its monolayer over 1000 trials).  Each trial has its
+    own x, dL/dy and output buffers, up to 1 GiB in total, then they repeat."""
+    import torch
+
+    from paper_2408_00280_amd import native
+    esz = x0.element_size()
+    per = T * N * 3 * esz + T * row + sbytes
+    R = max(1, min(trials, ROTATE_BYTES // per))
+    bufs = [{"x": x0.clone(), "gs": gs0.clone(), "g": torch.empty_like(gs0),
+             "spk": torch.empty((T, row), dtype=torch.uint8, device=dev),
+             "saved": torch.empty(sbytes, dtype=torch.uint8, device=dev) if sbytes else None} for _ in range(R)]
+    torch.cuda.synchronize()
+
+    def run():
+        s = torch.cuda.current_stream().cuda_stream   # the capture stream while capturing
+        for i in range(trials):
+            b = bufs[i % R]
+            native.snn_lif_forward(c, T, N, b["x"], b["spk"], b["saved"], None, s)
+            native.snn_lif_backward(c, T, N, b["x"], b["saved"], b["gs"], b["g"], s)
+
+    run()
+    eager_g = bufs[0]["g"].clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(bufs[0]["g"], eager_g), "graph replay differs from the eager run"
+    reps = 5
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    nbytes = (bpn["lif_forward"] + bpn["lif_backward"]) * T * N * trials
+    return {"trials": trials, "buffer_sets": R, "ms_per_replay": ms, "us_per_trial": ms * 1e3 / trials,
+            "value": trials * T * N / (ms * 1e-3), "unit": "neuron-timesteps/s",
+            "hbm_fraction": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "note": "forward+backward pairs replayed from one HIP graph; not the per-call figure"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,6 +256,9 @@ def main():
     ap.add_argument("--T", type=int, default=None, help="override T (large workload sweep)")
     ap.add_argument("--fused-stack", action="store_true",
                     help="stack: layers after the first read the previous spikes through the gain")
+    ap.add_argument("--graph-trials", type=int, default=None,
+                    help="also time this many independent forward+backward trials replayed from one HIP "
+                         "graph (default 1000 for the single workload, else off)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--with-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration runs)")
@@ -361,6 +448,9 @@ def main():
         "kernels": kernels,
         "kernel_source_sha256_16": source_hash(),
     }
+    trials = args.graph_trials if args.graph_trials is not None else (1000 if w.name == "single" else 0)
+    if trials and L == 1:
+        out["graph_trials"] = graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev)
     if not args.no_cpu_baseline:
         if keep_host:
             x_np, gs_np = np.concatenate(host["x"]), np.concatenate(host["gs"])

@@ -107,6 +107,29 @@ snn_status snn_lif_forward(const snn_lif_cfg *cfg, int64_t T, int64_t N, const v
 snn_status snn_lif_backward(const snn_lif_cfg *cfg, int64_t T, int64_t N, const void *x,
                             const void *saved, const void *grad_s, void *grad_x, void *stream);
 
+/* The same layer over one time segment of a longer sequence: the state handoff of the
+ * temporal split (Sec. 3.3, Fig. 1(b)), where consecutive segments of one layer run one
+ * after the other (on one GPU, or on neighbouring GPUs with the four [N] fp32 vectors
+ * below exchanged between them).  Running a sequence as segments T = T_1 + T_2 + ...
+ * with the handoff gives the same spikes, membranes and gradients, bit for bit, as one
+ * call over all T.  Each of the four pointers may be NULL; all are [N] float32, 16-byte
+ * aligned, device memory:
+ *   v_in    the membrane the preceding segment ended with (its v_last): v^0 of this
+ *           segment, whose spike state is taken as v_in >= V_th (Eq. (2)).  NULL: the
+ *           sequence starts here (v^0 = V_rest, no spike).
+ *   v_last  out: the membrane after the segment's last step, v^T.
+ *   g_in    dL/dv^{T+1}, handed back by the following segment (its g_out).  NULL: 0, the
+ *           sequence ends here.
+ *   g_out   out: dL/dv^1 of this segment in fp32 (= dL/dx^1 before rounding to cfg->io).
+ * forward_seg / backward_seg of one segment must get the same v_in.  With T == 0 nothing
+ * is written.  snn_lif_forward / snn_lif_backward are these calls with all four NULL. */
+snn_status snn_lif_forward_seg(const snn_lif_cfg *cfg, int64_t T, int64_t N, const void *x,
+                               const float *v_in, void *spikes, void *saved, float *v_last,
+                               float *v_out, void *stream);
+snn_status snn_lif_backward_seg(const snn_lif_cfg *cfg, int64_t T, int64_t N, const void *x,
+                                const float *v_in, const void *saved, const void *grad_s,
+                                const float *g_in, void *grad_x, float *g_out, void *stream);
+
 /* Stand-in for the ANN operator between stacked LIF layers (not part of the paper's
  * method): a per-feature gain, N = B*F neurons per step, neuron (b, f) at b*F + f.
  *   forward:  x_next[t][b][f] = gain[f] * y[t][b][f]   (spikes in cfg->spk format,

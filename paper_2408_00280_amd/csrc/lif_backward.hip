@@ -17,22 +17,25 @@ namespace snnlif {
 
 template <int IO>
 snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
-                          const void* saved, const void* gs, void* gx, hipStream_t s) {
+                          const void* saved, const void* gs, void* gx, const float* v_in, const float* g_in,
+                          float* g_out, hipStream_t s) {
     const float* sv = static_cast<const float*>(saved);
+    const BwdSeg seg{v_in, g_in, g_out};
     auto go = [&](auto rst) {
         return backward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
             return launch(lif_backward_kernel<IO, R, Vc, Kc, Pc>, grid_for((N + Vc - 1) / Vc), s, k, T, N, x, sv,
-                          gs, gx);
+                          gs, gx, seg);
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});
 }
 
 template snn_status backward_entry<SNNLIF_IO>(int, const Plan&, const LifK&, int64_t, int64_t, const void*,
-                                              const void*, const void*, void*, hipStream_t);
+                                              const void*, const void*, void*, const float*, const float*, float*,
+                                              hipStream_t);
 
 #else
 

@@ -18,7 +18,8 @@ namespace snnlif {
 
 template <int IO, int SPK>
 snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
-                         void* spikes, void* saved, float* v_out, hipStream_t s) {
+                         void* spikes, void* saved, float* v_out, const float* v_in, float* v_last,
+                         hipStream_t s) {
     uint8_t* sp = static_cast<uint8_t*>(spikes);
     float* sv = static_cast<float*>(saved);
     const dim3 g = grid_for(p.lanes);
@@ -28,16 +29,17 @@ snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
             return v_out ? launch(lif_forward_kernel<IO, SPK, R, Vc, Kc, true, Pc>, g, s, k, T, N, x, sp,
-                                  p.row_bytes, sv, v_out)
+                                  p.row_bytes, sv, v_out, v_in, v_last)
                          : launch(lif_forward_kernel<IO, SPK, R, Vc, Kc, false, Pc>, g, s, k, T, N, x, sp,
-                                  p.row_bytes, sv, v_out);
+                                  p.row_bytes, sv, v_out, v_in, v_last);
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});
 }
 
 template snn_status forward_entry<SNNLIF_IO, SNNLIF_SPK>(int, const Plan&, const LifK&, int64_t, int64_t,
-                                                         const void*, void*, void*, float*, hipStream_t);
+                                                         const void*, void*, void*, float*, const float*, float*,
+                                                         hipStream_t);
 
 #else
 

@@ -149,13 +149,17 @@ snn_status backward_variant(const Plan& p, F&& f) {
 }
 
 // Launchers, one per kernel translation unit (defined by explicit instantiation there).
+// v_in / v_last / g_in / g_out: the segment state of a sequence split along time (each may
+// be null; see snn_lif_forward_seg and snn_lif_backward_seg).
 template <int IO, int SPK>
 snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
-                         void* spikes, void* saved, float* v_out, hipStream_t s);
+                         void* spikes, void* saved, float* v_out, const float* v_in, float* v_last,
+                         hipStream_t s);
 
 template <int IO>
 snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, const void* x,
-                          const void* saved, const void* gs, void* gx, hipStream_t s);
+                          const void* saved, const void* gs, void* gx, const float* v_in, const float* g_in,
+                          float* g_out, hipStream_t s);
 
 // The layer fed by the previous layer's spikes (format SPK, u8 or bits) through a per-feature
 // gain of F features.

@@ -302,7 +302,14 @@ __device__ __forceinline__ void store_f32(float* p, const float (&f)[V]) {
 
 template <int V>
 __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
-    if constexpr (V == 4) {
+    if constexpr (V == 8) {
+        const f32x4_t a = ld_nt<f32x4_t>(p), b = ld_nt<f32x4_t>(p + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f[j] = a[j];
+            f[4 + j] = b[j];
+        }
+    } else if constexpr (V == 4) {
         const f32x4_t a = ld_nt<f32x4_t>(p);
         f[0] = a[0];
         f[1] = a[1];
@@ -407,10 +414,14 @@ __device__ __forceinline__ void forward_rows(const LifK& c, const In& in, const 
 // checkpointed to saved[chunk][N].  PIPE: double-buffered chunks -- the next chunk's rows
 // are in flight while the current chunk is computed (for layers with few lanes, where
 // occupancy alone cannot hide the memory latency).
+// Segment state (a sequence split along time): v_in, if not null, is the membrane the
+// previous segment ended with, and the spike state entering the first step is v_in >= V_th;
+// v_last, if not null, receives the membrane after the last step.
 template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE, bool ALL, typename In>
 __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
                                               uint8_t* __restrict__ spikes, int64_t row_bytes,
-                                              float* __restrict__ saved, float* __restrict__ v_out) {
+                                              float* __restrict__ saved, float* __restrict__ v_out,
+                                              const float* __restrict__ v_in, float* __restrict__ v_last) {
     using raw = typename In::raw;
     const bool active = ALL || n0 < N;
     float v[V];
@@ -419,6 +430,11 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
     for (int j = 0; j < V; ++j) {
         v[j] = c.rest;  // v^0 = V_rest
         y[j] = false;   // no spike before the first step
+    }
+    if (v_in != nullptr && (ALL || active)) {
+        load_f32<V>(v_in + n0, v);
+#pragma unroll
+        for (int j = 0; j < V; ++j) y[j] = v[j] >= c.th;
     }
     const int64_t n_full = T / K;
     const int k_tail = int(T % K);
@@ -477,6 +493,7 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
         forward_rows<IO, SPK, RESET, V, K, VOUT, false, ALL>(c, in, a, N, n_full * K, k_tail, n0, active, spikes,
                                                              row_bytes, v_out, v, y);
     }
+    if (v_last != nullptr && (ALL || active)) store_f32<V>(v_last + n0, v);
 }
 
 // Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
@@ -487,14 +504,18 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
                                                              uint8_t* __restrict__ spikes,
                                                              int64_t row_bytes,
                                                              float* __restrict__ saved,
-                                                             float* __restrict__ v_out) {
+                                                             float* __restrict__ v_out,
+                                                             const float* __restrict__ v_in,
+                                                             float* __restrict__ v_last) {
     const int64_t first = xcd_contiguous_block() * kBlock * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
     const DenseIn<IO, V> in{x};
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+                                                              v_in, v_last);
     else
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+                                                               v_in, v_last);
 }
 
 // The same forward with the input current read from the previous layer's spikes through
@@ -514,9 +535,11 @@ __global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_
     in.row_bytes = row_bytes;
     in.init(gain, F, n0, n0 < N);
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+                                                              nullptr, nullptr);
     else
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out);
+        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+                                                               nullptr, nullptr);
 }
 
 // Backward of one chunk.  v/y enter as the state before the chunk's first step; g enters
@@ -573,19 +596,31 @@ struct BwdChunk {
     float v[V];
 };
 
+// Segment state of the backward (a sequence split along time): v_in as in the forward;
+// g_in, if not null, is dL/dv^{T+1}, the gradient the following segment hands back (else
+// 0); g_out, if not null, receives dL/dv^1 in fp32 for the preceding segment.
+struct BwdSeg {
+    const float* v_in;
+    const float* g_in;
+    float* g_out;
+};
+
 // ALWAYS: the layer has a checkpoint row, so the state is loaded unconditionally (chunk 0
-// reads row 0 and then takes V_rest instead), keeping the caller's loop free of branches.
+// reads v_in, or row 0 and then takes V_rest instead), keeping the caller's loop free of
+// branches.
 template <int IO, int V, int K, bool FULL, bool ALWAYS, typename In>
 __device__ __forceinline__ void backward_load(BwdChunk<IO, V, K, In>& b, const LifK& c, const In& in,
-                                              const float* __restrict__ saved, const void* gs, int64_t N,
-                                              int64_t ch, int kn, int64_t n0) {
+                                              const float* __restrict__ saved, const float* v_in, const void* gs,
+                                              int64_t N, int64_t ch, int kn, int64_t n0) {
     if (ALWAYS) {
-        load_f32<V>(saved + (ch > 0 ? ch - 1 : 0) * N + n0, b.v);
-    } else if (ch == 0) {
+        load_f32<V>((ch > 0 ? saved + (ch - 1) * N : v_in != nullptr ? v_in : saved) + n0, b.v);
+    } else if (ch > 0) {
+        load_f32<V>(saved + (ch - 1) * N + n0, b.v);
+    } else if (v_in != nullptr) {
+        load_f32<V>(v_in + n0, b.v);
+    } else {
 #pragma unroll
         for (int j = 0; j < V; ++j) b.v[j] = c.rest;
-    } else {
-        load_f32<V>(saved + (ch - 1) * N + n0, b.v);
     }
     load_rows<In, K, FULL, false>(in, b.x, N, ch * K, kn, n0);
     load_rows<DenseIn<IO, V>, K, FULL, true>(DenseIn<IO, V>{gs}, b.gs, N, ch * K, kn, n0);
@@ -593,13 +628,17 @@ __device__ __forceinline__ void backward_load(BwdChunk<IO, V, K, In>& b, const L
 
 template <int IO, int RESET, int V, int K, bool FULL, bool GAIN, typename In>
 __device__ __forceinline__ void backward_chunk(const LifK& c, const In& in, const BwdChunk<IO, V, K, In>& b,
-                                               int64_t N, int64_t ch, int kn, int64_t n0, void* gx, float (&g)[V]) {
+                                               bool has_v_in, int64_t N, int64_t ch, int kn, int64_t n0, void* gx,
+                                               float (&g)[V]) {
+    // a checkpoint (or v_in) is a post-step membrane with spike state v >= V_th; the
+    // sequence itself starts at V_rest with no spike
+    const bool carried = ch > 0 || has_v_in;
     float v[V];
     bool y[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) {
-        v[j] = ch > 0 ? b.v[j] : c.rest;
-        y[j] = ch > 0 && b.v[j] >= c.th;  // a checkpoint is a post-step membrane; step 0 has y = 0
+        v[j] = carried ? b.v[j] : c.rest;
+        y[j] = carried && b.v[j] >= c.th;
     }
     backward_rows<IO, RESET, V, K, FULL, GAIN>(c, in, b.x, b.gs, N, ch * K, kn, n0, gx, v, y, g);
 }
@@ -607,25 +646,31 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, const In& in, cons
 // Chunks are processed last-first: the short tail chunk (if any), then the full chunks.
 template <int IO, int RESET, int V, int K, bool PIPE, bool GAIN, typename In>
 __device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
-                                               const float* __restrict__ saved, const void* gs, void* gx) {
+                                               const float* __restrict__ saved, const void* gs, void* gx,
+                                               const BwdSeg& seg) {
     using Chunk = BwdChunk<IO, V, K, In>;
     float g[V];
+    if (seg.g_in != nullptr) {
+        load_f32<V>(seg.g_in + n0, g);
+    } else {
 #pragma unroll
-    for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
+        for (int j = 0; j < V; ++j) g[j] = 0.0f;  // dL/dv^{T+1} = 0
+    }
+    const bool has_v_in = seg.v_in != nullptr;
     const int64_t n_full = T / K;
     const int k_tail = int(T % K);
     Chunk a;
     if (k_tail) {
-        backward_load<IO, V, K, false, false>(a, c, in, saved, gs, N, n_full, k_tail, n0);
-        backward_chunk<IO, RESET, V, K, false, GAIN>(c, in, a, N, n_full, k_tail, n0, gx, g);
+        backward_load<IO, V, K, false, false>(a, c, in, saved, seg.v_in, gs, N, n_full, k_tail, n0);
+        backward_chunk<IO, RESET, V, K, false, GAIN>(c, in, a, has_v_in, N, n_full, k_tail, n0, gx, g);
     }
     auto load = [&](Chunk& buf, int64_t ch) {
         __builtin_amdgcn_sched_barrier(0);
-        backward_load<IO, V, K, true, PIPE>(buf, c, in, saved, gs, N, ch, K, n0);
+        backward_load<IO, V, K, true, PIPE>(buf, c, in, saved, seg.v_in, gs, N, ch, K, n0);
         __builtin_amdgcn_sched_barrier(0);
     };
     auto step = [&](const Chunk& buf, int64_t ch) {
-        backward_chunk<IO, RESET, V, K, true, GAIN>(c, in, buf, N, ch, K, n0, gx, g);
+        backward_chunk<IO, RESET, V, K, true, GAIN>(c, in, buf, has_v_in, N, ch, K, n0, gx, g);
     };
     if constexpr (!PIPE) {
         for (int64_t ch = n_full - 1; ch >= 0; --ch) {
@@ -657,17 +702,18 @@ __device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int6
             }
         }
     }
+    if (seg.g_out != nullptr) store_f32<V>(seg.g_out + n0, g);
 }
 
 template <int IO, int RESET, int V, int K, bool PIPE>
 __global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
                                                               const void* __restrict__ x,
                                                               const float* __restrict__ saved,
-                                                              const void* gs, void* gx) {
+                                                              const void* gs, void* gx, BwdSeg seg) {
     const int64_t first = xcd_contiguous_block() * kBlock * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
     if (first + kBlock * V > N && n0 >= N) return;
-    backward_lanes<IO, RESET, V, K, PIPE, false>(c, DenseIn<IO, V>{x}, T, N, n0, saved, gs, gx);
+    backward_lanes<IO, RESET, V, K, PIPE, false>(c, DenseIn<IO, V>{x}, T, N, n0, saved, gs, gx, seg);
 }
 
 // Backward of the gain-fed layer: recomputes from the previous layer's spikes and writes
@@ -686,7 +732,7 @@ __global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64
     in.s = spikes_in;
     in.row_bytes = row_bytes;
     in.init(gain, F, n0, true);
-    backward_lanes<IO, RESET, V, K, PIPE, true>(c, in, T, N, n0, saved, gs, gs_in);
+    backward_lanes<IO, RESET, V, K, PIPE, true>(c, in, T, N, n0, saved, gs, gs_in, BwdSeg{nullptr, nullptr, nullptr});
 }
 
 // ------------------------------------------------------------------------------------

@@ -7,19 +7,26 @@ using namespace snnlif;
 namespace {
 
 snn_status forward_dispatch(const snn_lif_cfg* c, const Plan& p, const LifK& k, int64_t T, int64_t N,
-                            const void* x, void* spikes, void* saved, float* v_out, hipStream_t s) {
+                            const void* x, void* spikes, void* saved, float* v_out, const float* v_in,
+                            float* v_last, hipStream_t s) {
     const int r = c->reset;
     if (c->io == SNN_IO_F32) {
         switch (c->spk) {
-            case SNN_SPK_U8: return forward_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, x, spikes, saved, v_out, s);
-            case SNN_SPK_BITS: return forward_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, x, spikes, saved, v_out, s);
-            default: return forward_entry<SNN_IO_F32, SNN_SPK_IO>(r, p, k, T, N, x, spikes, saved, v_out, s);
+            case SNN_SPK_U8:
+                return forward_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
+            case SNN_SPK_BITS:
+                return forward_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
+            default:
+                return forward_entry<SNN_IO_F32, SNN_SPK_IO>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
         }
     }
     switch (c->spk) {
-        case SNN_SPK_U8: return forward_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, x, spikes, saved, v_out, s);
-        case SNN_SPK_BITS: return forward_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, x, spikes, saved, v_out, s);
-        default: return forward_entry<SNN_IO_BF16, SNN_SPK_IO>(r, p, k, T, N, x, spikes, saved, v_out, s);
+        case SNN_SPK_U8:
+            return forward_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
+        case SNN_SPK_BITS:
+            return forward_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
+        default:
+            return forward_entry<SNN_IO_BF16, SNN_SPK_IO>(r, p, k, T, N, x, spikes, saved, v_out, v_in, v_last, s);
     }
 }
 
@@ -64,8 +71,8 @@ snn_status snn_lif_saved_bytes(const snn_lif_cfg* cfg, int64_t T, int64_t N, siz
     return SNN_OK;
 }
 
-snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, void* spikes,
-                           void* saved, float* v_out, void* stream) {
+snn_status snn_lif_forward_seg(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const float* v_in,
+                               void* spikes, void* saved, float* v_last, float* v_out, void* stream) {
     snn_status st = check_cfg(cfg);
     if (st != SNN_OK) return st;
     if ((st = check_shape(T, N)) != SNN_OK) return st;
@@ -73,14 +80,21 @@ snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const v
     const Plan p = make_plan(cfg, T, N);
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (x == nullptr || spikes == nullptr || (need_saved && saved == nullptr)) return SNN_E_NULL;
-    if (!aligned(x) || !aligned(spikes) || (saved && !aligned(saved)) || (v_out && !aligned(v_out)))
+    if (!aligned(x) || !aligned(spikes) || (saved && !aligned(saved)) || (v_out && !aligned(v_out)) ||
+        (v_in && !aligned(v_in)) || (v_last && !aligned(v_last)))
         return SNN_E_ALIGN;
-    return forward_dispatch(cfg, p, kernel_consts(cfg), T, N, x, spikes, need_saved ? saved : nullptr, v_out,
-                            static_cast<hipStream_t>(stream));
+    return forward_dispatch(cfg, p, kernel_consts(cfg), T, N, x, spikes, need_saved ? saved : nullptr, v_out, v_in,
+                            v_last, static_cast<hipStream_t>(stream));
 }
 
-snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const void* saved,
-                            const void* grad_s, void* grad_x, void* stream) {
+snn_status snn_lif_forward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, void* spikes,
+                           void* saved, float* v_out, void* stream) {
+    return snn_lif_forward_seg(cfg, T, N, x, nullptr, spikes, saved, nullptr, v_out, stream);
+}
+
+snn_status snn_lif_backward_seg(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const float* v_in,
+                                const void* saved, const void* grad_s, const float* g_in, void* grad_x,
+                                float* g_out, void* stream) {
     snn_status st = check_cfg(cfg);
     if (st != SNN_OK) return st;
     if ((st = check_shape(T, N)) != SNN_OK) return st;
@@ -89,12 +103,20 @@ snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const 
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (x == nullptr || grad_s == nullptr || grad_x == nullptr || (need_saved && saved == nullptr))
         return SNN_E_NULL;
-    if (!aligned(x) || !aligned(grad_s) || !aligned(grad_x) || (saved && !aligned(saved))) return SNN_E_ALIGN;
+    if (!aligned(x) || !aligned(grad_s) || !aligned(grad_x) || (saved && !aligned(saved)) ||
+        (v_in && !aligned(v_in)) || (g_in && !aligned(g_in)) || (g_out && !aligned(g_out)))
+        return SNN_E_ALIGN;
     const LifK k = kernel_consts(cfg);
     hipStream_t s = static_cast<hipStream_t>(stream);
     const void* sv = need_saved ? saved : nullptr;
-    return cfg->io == SNN_IO_F32 ? backward_entry<SNN_IO_F32>(cfg->reset, p, k, T, N, x, sv, grad_s, grad_x, s)
-                                 : backward_entry<SNN_IO_BF16>(cfg->reset, p, k, T, N, x, sv, grad_s, grad_x, s);
+    return cfg->io == SNN_IO_F32
+               ? backward_entry<SNN_IO_F32>(cfg->reset, p, k, T, N, x, sv, grad_s, grad_x, v_in, g_in, g_out, s)
+               : backward_entry<SNN_IO_BF16>(cfg->reset, p, k, T, N, x, sv, grad_s, grad_x, v_in, g_in, g_out, s);
+}
+
+snn_status snn_lif_backward(const snn_lif_cfg* cfg, int64_t T, int64_t N, const void* x, const void* saved,
+                            const void* grad_s, void* grad_x, void* stream) {
+    return snn_lif_backward_seg(cfg, T, N, x, nullptr, saved, grad_s, nullptr, grad_x, nullptr, stream);
 }
 
 snn_status snn_gain_spikes_forward(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes,

@@ -52,23 +52,34 @@ def alloc_forward(cfg: LifConfig, T: int, N: int, device, v_out: bool = False):
     return spikes, saved, v
 
 
-def forward(cfg: LifConfig, x: torch.Tensor, *, v_out: bool = False, out=None, stream=None):
-    """Fused forward of x[T, ...] (cfg.dtype, contiguous).  Returns (spikes, saved, v_or_None)."""
+def forward(cfg: LifConfig, x: torch.Tensor, *, v_out: bool = False, out=None, v_in=None, v_last=None,
+            stream=None):
+    """Fused forward of x[T, ...] (cfg.dtype, contiguous).  Returns (spikes, saved, v_or_None).
+    v_in / v_last ([N] float32): segment state of a sequence split along time."""
     assert x.dtype == cfg.dtype and x.is_contiguous()
     T, N = _TN(x)
     spikes, saved, v = out if out is not None else alloc_forward(cfg, T, N, x.device, v_out)
-    native.snn_lif_forward(cfg.c(), T, N, x, spikes, saved if saved.numel() else None, v, stream)
+    sv = saved if saved.numel() else None
+    if v_in is None and v_last is None:
+        native.snn_lif_forward(cfg.c(), T, N, x, spikes, sv, v, stream)
+    else:
+        native.snn_lif_forward_seg(cfg.c(), T, N, x, v_in, spikes, sv, v_last, v, stream)
     return spikes, saved, v
 
 
 def backward(cfg: LifConfig, x: torch.Tensor, saved: torch.Tensor, grad_s: torch.Tensor, *,
-             grad_x: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    """Fused backward; returns dL/dx with x's shape and dtype (in place if grad_x is grad_s)."""
+             grad_x: torch.Tensor | None = None, v_in=None, g_in=None, g_out=None, stream=None) -> torch.Tensor:
+    """Fused backward; returns dL/dx with x's shape and dtype (in place if grad_x is grad_s).
+    v_in / g_in / g_out ([N] float32): segment state of a sequence split along time."""
     assert grad_s.dtype == cfg.dtype and grad_s.shape == x.shape and grad_s.is_contiguous()
     T, N = _TN(x)
     if grad_x is None:
         grad_x = torch.empty_like(grad_s)
-    native.snn_lif_backward(cfg.c(), T, N, x, saved if saved.numel() else None, grad_s, grad_x, stream)
+    sv = saved if saved.numel() else None
+    if v_in is None and g_in is None and g_out is None:
+        native.snn_lif_backward(cfg.c(), T, N, x, sv, grad_s, grad_x, stream)
+    else:
+        native.snn_lif_backward_seg(cfg.c(), T, N, x, v_in, sv, grad_s, g_in, grad_x, g_out, stream)
     return grad_x
 
 

@@ -29,6 +29,7 @@ STATUS_NAMES = {0: "SNN_OK", -1: "SNN_E_NULL", -2: "SNN_E_SHAPE", -3: "SNN_E_PAR
 
 # Every symbol the header declares; a test checks the library exports all of them.
 EXPORTS = ("snn_spike_row_bytes", "snn_lif_saved_bytes", "snn_lif_forward", "snn_lif_backward",
+           "snn_lif_forward_seg", "snn_lif_backward_seg",
            "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_lif_forward_gain",
            "snn_lif_backward_gain", "snn_lif_serial_forward_step",
            "snn_lif_serial_backward_step", "snn_status_str")
@@ -67,6 +68,8 @@ def _load():
         "snn_lif_saved_bytes": [C, i64, i64, szp],
         "snn_lif_forward": [C, i64, i64, vp, vp, vp, vp, vp],
         "snn_lif_backward": [C, i64, i64, vp, vp, vp, vp, vp],
+        "snn_lif_forward_seg": [C, i64, i64, vp, vp, vp, vp, vp, vp, vp],
+        "snn_lif_backward_seg": [C, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp],
         "snn_gain_spikes_forward": [C, i64, i64, i64, vp, vp, vp, vp],
         "snn_gain_grad_backward": [C, i64, i64, i64, vp, vp, vp, vp],
         "snn_lif_forward_gain": [C, i64, i64, i64, vp, vp, vp, vp, vp, vp],
@@ -133,6 +136,18 @@ def snn_lif_forward(cfg, T, N, x, spikes, saved, v_out=None, stream=None):
 def snn_lif_backward(cfg, T, N, x, saved, grad_s, grad_x, stream=None):
     _check("snn_lif_backward", lib.snn_lif_backward(ctypes.byref(cfg), T, N, _ptr(x), _ptr(saved),
                                                     _ptr(grad_s), _ptr(grad_x), _stream(stream)))
+
+
+def snn_lif_forward_seg(cfg, T, N, x, v_in, spikes, saved, v_last=None, v_out=None, stream=None):
+    _check("snn_lif_forward_seg", lib.snn_lif_forward_seg(
+        ctypes.byref(cfg), T, N, _ptr(x), _ptr(v_in), _ptr(spikes), _ptr(saved), _ptr(v_last), _ptr(v_out),
+        _stream(stream)))
+
+
+def snn_lif_backward_seg(cfg, T, N, x, v_in, saved, grad_s, g_in, grad_x, g_out=None, stream=None):
+    _check("snn_lif_backward_seg", lib.snn_lif_backward_seg(
+        ctypes.byref(cfg), T, N, _ptr(x), _ptr(v_in), _ptr(saved), _ptr(grad_s), _ptr(g_in), _ptr(grad_x),
+        _ptr(g_out), _stream(stream)))
 
 
 def snn_gain_spikes_forward(cfg, T, B, F, spikes, gain, x_next, stream=None):

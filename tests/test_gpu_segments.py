@@ -1,0 +1,135 @@
+"""GPU tests of the segment state handoff (snn_lif_forward_seg / snn_lif_backward_seg): a
+sequence split along time into consecutive segments, each handing its last membrane
+forward and its first-step gradient back, must reproduce the single call over all T bit
+for bit (the temporal split of a layer), and a segment started from an arbitrary state
+must match the oracle started from the same state."""
+import itertools
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def H():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_harness
+    return gpu_harness
+
+
+COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits", "io"]))
+
+# (T, N, segment lengths): single- and multi-chunk segments, tails, one-step segments,
+# and layer sizes that reach the 4-, 2- and 1-neuron lanes and double buffering.
+SPLITS = [
+    (2, 1000, [1, 1]),
+    (40, 4097, [17, 23]),
+    (64, 20000, [1, 31, 32]),
+    (100, 70001, [50, 50]),
+    (40, (1 << 20) + 4, [8, 9, 23]),
+    (48, 1 << 21, [16, 32]),
+]
+
+
+def _segments_vs_whole(H, w, lens):
+    torch = H.torch
+    cfg = H.cfg_of(w)
+    T, N = w.T, w.N
+    x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+    x, gs = H.to_dev(x_np, w.io), H.to_dev(gs_np, w.io)
+    spikes, saved, v = H.layer.forward(cfg, x, v_out=True)
+    gx = H.layer.backward(cfg, x, saved, gs)
+
+    bounds = np.cumsum([0] + lens)
+    assert bounds[-1] == T
+    states = []
+    v_in = None
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        xs = x[a:b].clone()   # its own allocation: a row slice of x is not 16-byte aligned in general
+        v_last = torch.empty(N, dtype=torch.float32, device=H.DEV)
+        s_seg, sv_seg, v_seg = H.layer.forward(cfg, xs, v_out=True, v_in=v_in, v_last=v_last)
+        assert torch.equal(s_seg, spikes[a:b]), f"spikes of segment [{a}, {b})"
+        assert torch.equal(v_seg, v[a:b]), f"membranes of segment [{a}, {b})"
+        assert torch.equal(v_last, v[b - 1]), f"v_last of segment [{a}, {b})"
+        states.append((a, b, xs, sv_seg, v_in))
+        v_in = v_last
+    g_in = None
+    for a, b, xs, sv_seg, vi in reversed(states):
+        g_out = torch.empty(N, dtype=torch.float32, device=H.DEV)
+        gx_seg = H.layer.backward(cfg, xs, sv_seg, gs[a:b].clone(), v_in=vi, g_in=g_in, g_out=g_out)
+        assert torch.equal(gx_seg, gx[a:b]), f"dL/dx of segment [{a}, {b})"
+        assert torch.equal(g_out.to(gx.dtype), gx[a]), f"g_out of segment [{a}, {b})"
+        g_in = g_out
+    torch.cuda.synchronize()
+    # the whole run itself against the oracle
+    rep, _ = H.compare_layer(w, spikes, v, gx, x_np, gs_np)
+    return rep
+
+
+@pytest.mark.parametrize("T,N,lens", SPLITS, ids=lambda v: str(v))
+@pytest.mark.parametrize("reset,io,spk", COMBOS, ids=lambda v: str(v))
+def test_segments_equal_whole(H, T, N, lens, reset, io, spk):
+    p = H.W.LifParams(0.5, 1.0, reset=reset)
+    w = H.W.custom(f"seg{T}x{N}", T, N, p, seed=T + N, io=io, spk=spk, x_dist=("normal", 0.5, 0.5))
+    rep = _segments_vs_whole(H, w, lens)
+    assert rep.ok(), str(rep)
+    H.torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("reset,io", list(itertools.product(["hard", "soft"], ["f32", "bf16"])))
+def test_segment_from_arbitrary_state(H, reset, io):
+    """v_in with values above and below V_th (spiking and not), NaN and +inf, and a
+    nonzero g_in, against the oracle started from the same state."""
+    torch = H.torch
+    T, N = 37, 5003
+    rng = np.random.default_rng(3)
+    p = H.W.LifParams(0.75, 1.0, v_reset=0.125, alpha=2.0, reset=reset)
+    w = H.W.custom("segstate", T, N, p, seed=9, io=io, x_dist=("normal", 0.3, 0.5))
+    cfg = H.cfg_of(w)
+    x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+    v_in = rng.normal(0.8, 0.6, size=N).astype(np.float32)
+    v_in[:4] = [1.0, np.nextafter(np.float32(1.0), np.float32(0.0)), np.inf, np.nan]
+    g_in = rng.normal(size=N).astype(np.float32)
+    v_last = torch.empty(N, dtype=torch.float32, device=H.DEV)
+    g_out = torch.empty(N, dtype=torch.float32, device=H.DEV)
+    x, gs = H.to_dev(x_np, io), H.to_dev(gs_np, io)
+    vi, gi = torch.from_numpy(v_in).to(H.DEV), torch.from_numpy(g_in).to(H.DEV)
+    spikes, saved, v = H.layer.forward(cfg, x, v_out=True, v_in=vi, v_last=v_last)
+    gx = H.layer.backward(cfg, x, saved, gs, v_in=vi, g_in=gi, g_out=g_out)
+    torch.cuda.synchronize()
+
+    op = H.oracle.Params.of(w.params)
+    y_ref, v_ref = H.oracle.forward(op, x_np, v_init=v_in, y_init=(v_in >= np.float32(1.0)).astype(np.uint8))
+    g_ref, bound = H.oracle.backward(op, v_ref, y_ref, gs_np, g_next=g_in)
+    y_gpu = H.parity.unpack_spikes(spikes.cpu().numpy(), N, w.spk)
+    rep = H.parity.compare_forward(y_gpu, y_ref, v_ref, 1.0, v_gpu=v.cpu().numpy())
+    rtol = H.parity.RTOL_BF16 if io == "bf16" else H.parity.RTOL_F32
+    H.parity.compare_grad(H.to_host_f32(gx), g_ref, bound, rtol, rep)
+    H.parity.compare_grad(g_out.cpu().numpy()[None, :], g_ref[:1], bound[:1], H.parity.RTOL_F32, rep)
+    assert rep.ok(), str(rep)
+    assert np.array_equal(v_last.cpu().numpy().view(np.uint32), v_ref[-1].view(np.uint32))
+
+
+def test_segment_errors(H):
+    torch = H.torch
+    nat = H.native
+    cfg = H.layer.LifConfig(0.5, 1.0)
+    T, N = 4, 64
+    x = torch.zeros((T, N), device=H.DEV)
+    sp = torch.empty((T, N), dtype=torch.uint8, device=H.DEV)
+    st = torch.zeros(N + 4, device=H.DEV)
+    with pytest.raises(nat.SnnError) as e:
+        nat.snn_lif_forward_seg(cfg.c(), T, N, x, st.data_ptr() + 4, sp, None)
+    assert e.value.status == -4
+    with pytest.raises(nat.SnnError) as e:
+        nat.snn_lif_backward_seg(cfg.c(), T, N, x, None, None, x, st.data_ptr() + 4, x)
+    assert e.value.status == -4
+    # empty segments write nothing
+    keep = torch.full((N,), 7.0, device=H.DEV)
+    nat.snn_lif_forward_seg(cfg.c(), 0, N, None, None, None, None, keep)
+    nat.snn_lif_backward_seg(cfg.c(), 0, N, None, None, None, None, None, None, keep)
+    torch.cuda.synchronize()
+    assert bool((keep == 7.0).all())
