@@ -201,6 +201,14 @@ def compare_serial(args):
         torch.cuda.empty_cache()
 
 
+def system_info(torch) -> dict:
+    """The device and software the numbers were taken on."""
+    props = torch.cuda.get_device_properties(0)
+    return {"device": props.name, "arch": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count, "hbm_bytes": props.total_memory,
+            "hip": torch.version.hip, "torch": torch.__version__}
+
+
 def graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev):
     """`trials` independent forward+backward pairs of one layer, captured into one HIP graph
     and replayed (the paper measures its monolayer over 1000 trials).  Each trial has its
@@ -403,7 +411,8 @@ def main():
     kernels = {}
     for name, d in per.items():
         ms = float(np.mean(d["ms"]))
-        kernels[name + "_kernel"] = {"avg_launch_ms": ms, "launches_per_step": len(d["ms"]) // K,
+        kernels[name + "_kernel"] = {"avg_launch_ms": ms, "median_launch_ms": float(np.median(d["ms"])),
+                                     "launches_per_step": len(d["ms"]) // K,
                                      "GB/s": d["bytes"] / (ms * 1e-3) / 1e9,
                                      "bytes_per_nts": bpn[name]}
     step_kernel_ms = sum(v["avg_launch_ms"] * v["launches_per_step"] for v in kernels.values())
@@ -447,6 +456,7 @@ def main():
                      "bytes_per_nts": dom["bytes_per_nts"], "avg_launch_ms": dom["avg_launch_ms"]},
         "kernels": kernels,
         "kernel_source_sha256_16": source_hash(),
+        "system": system_info(torch),
     }
     trials = args.graph_trials if args.graph_trials is not None else (1000 if w.name == "single" else 0)
     if trials and L == 1:
