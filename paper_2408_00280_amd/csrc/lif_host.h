@@ -58,6 +58,11 @@ constexpr int chunk_steps(int io, int v, bool pipe) {
     return v == 4 ? (pipe && io == SNN_IO_F32 ? 8 : 16) : v == 2 ? 16 : 32;
 }
 
+// A layer of T <= K steps is one chunk and keeps no checkpoint; it runs with the shortest
+// of these chunk lengths that holds T, so that registers sized for K steps do not cap the
+// occupancy of short-lived waves.
+constexpr int kShortChunks[] = {4, 8, 16};
+
 // Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
 constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 
@@ -67,6 +72,14 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     if (p.vb == 4 && N / 4 < kFillLanes) p.vb = 2;   // twice the lanes for small layers
     p.pipe = T > chunk_steps(c->io, p.vb, false) && N / p.vb < 4 * kFillLanes;
     p.k = chunk_steps(c->io, p.vb, p.pipe);
+    if (T <= p.k) {
+        for (int k : kShortChunks) {
+            if (T <= k && k < p.k) {
+                p.k = k;
+                break;
+            }
+        }
+    }
     // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
     p.vf = (c->io == SNN_IO_BF16 && p.vb == 4 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
     p.row_bytes = spike_row_bytes(c, N);
@@ -116,10 +129,28 @@ snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
 template <int I>
 using IntC = std::integral_constant<int, I>;
 
+// The single-chunk layers of kShortChunks (never double-buffered).
+template <int V, typename F>
+snn_status short_variant(const Plan& p, F&& f) {
+    switch (p.k) {
+        case 4: return f(IntC<V>{}, IntC<4>{}, std::false_type{});
+        case 8: return f(IntC<V>{}, IntC<8>{}, std::false_type{});
+        default: return f(IntC<V>{}, IntC<16>{}, std::false_type{});
+    }
+}
+
 template <int IO, typename F>
 snn_status forward_variant(const Plan& p, F&& f) {
     constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
     constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
+    if (!p.pipe && p.k < chunk_steps(IO, p.vb, false)) {
+        switch (p.vf) {
+            case 8: if constexpr (IO == SNN_IO_BF16) return short_variant<8>(p, f); else break;
+            case 4: return short_variant<4>(p, f);
+            case 2: return short_variant<2>(p, f);
+            default: return short_variant<1>(p, f);
+        }
+    }
     if constexpr (IO == SNN_IO_BF16) {
         if (p.vf == 8)   // 8-wide lanes keep the chunk of the 4-wide backward they pair with
             return p.pipe ? f(IntC<8>{}, IntC<K4p>{}, std::true_type{}) : f(IntC<8>{}, IntC<K4>{}, std::false_type{});
@@ -138,6 +169,13 @@ template <int IO, typename F>
 snn_status backward_variant(const Plan& p, F&& f) {
     constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
     constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
+    if (!p.pipe && p.k < chunk_steps(IO, p.vb, false)) {
+        switch (p.vb) {
+            case 4: return short_variant<4>(p, f);
+            case 2: return short_variant<2>(p, f);
+            default: return short_variant<1>(p, f);
+        }
+    }
     switch (p.vb * 2 + int(p.pipe)) {
         case 8: return f(IntC<4>{}, IntC<K4>{}, std::false_type{});
         case 9: return f(IntC<4>{}, IntC<K4p>{}, std::true_type{});

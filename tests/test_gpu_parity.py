@@ -21,7 +21,8 @@ def H():
 # ------------------------------------------------------------------ small random shapes
 
 SHAPES = [(1, 1), (1, 1000), (2, 3), (7, 63), (16, 64), (17, 65), (33, 1000), (40, 4097), (15, 1027),
-          (100, 256 * 4 * 3 + 4), (64, 70001)]
+          (100, 256 * 4 * 3 + 4), (64, 70001),
+          (4, 4097), (5, 64), (8, 1000), (12, 999)]   # the short single-chunk plans (4-, 8-, 16-step)
 PARAMS = {
     "k05": dict(decay=0.5, v_th=1.0),
     "paper": dict(decay=0.2, v_th=0.3),                 # Sec. 5.1 hyper-parameters
@@ -225,6 +226,11 @@ PLAN_SHAPES = [
     (40, 600002),           # 2 per lane, double-buffered, tail
     (40, 262145),           # 1 per lane (odd N), double-buffered 32-step chunks, tail
     (20, (1 << 20) + 1),    # 1 per lane, one chunk
+    (4, 1 << 20),           # short layers: one 4-step chunk, 4 per lane
+    (3, 1 << 21),           # 4-step chunk with a tail (bf16: 8 per lane in the forward)
+    (8, 524290),            # one 8-step chunk, 2 per lane
+    (6, 1 << 22),           # 8-step chunk with a tail, 4 per lane (bf16 forward: 8)
+    (12, 262145),           # one 16-step chunk at 1 per lane (whose long chunk is 32 steps)
 ]
 
 
