@@ -52,11 +52,10 @@ struct Plan {
     int64_t row_bytes;
 };
 
-// Steps per chunk: the backward keeps K membranes per neuron in VGPRs plus K rows of x and
-// dL/dy (twice the rows when double-buffered); bf16 rows take half the registers.
-constexpr int chunk_steps(int io, int v, bool pipe) {
-    return v == 4 ? (pipe && io == SNN_IO_F32 ? 8 : 16) : v == 2 ? 16 : 32;
-}
+// Steps per chunk for v neurons per backward lane: the backward keeps K membranes per
+// neuron in VGPRs plus K rows of x and dL/dy (twice the rows when double-buffered).  A
+// forward lane of 8 (bf16) pairs with a backward lane of 4.
+constexpr int chunk_steps(int v) { return v == 1 ? 32 : 16; }
 
 // A layer of T <= K steps is one chunk and keeps no checkpoint; it runs with the shortest
 // of these chunk lengths that holds T, so that registers sized for K steps do not cap the
@@ -68,10 +67,11 @@ constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 
 inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
-    p.vb = N % 4 == 0 ? 4 : N % 2 == 0 ? 2 : 1;
-    if (p.vb == 4 && N / 4 < kFillLanes) p.vb = 2;   // twice the lanes for small layers
-    p.pipe = T > chunk_steps(c->io, p.vb, false) && N / p.vb < 4 * kFillLanes;
-    p.k = chunk_steps(c->io, p.vb, p.pipe);
+    // fp32: 2 neurons per lane (8-byte rows; 4 per lane measured 1% slower on large
+    // layers); bf16: 4 per lane (8-byte rows) on layers that fill the chip, else 2
+    p.vb = N % 2 != 0 ? 1 : (c->io == SNN_IO_BF16 && N % 4 == 0 && N / 4 >= kFillLanes) ? 4 : 2;
+    p.pipe = T > chunk_steps(p.vb) && N / p.vb < 4 * kFillLanes;
+    p.k = chunk_steps(p.vb);
     if (T <= p.k) {
         for (int k : kShortChunks) {
             if (T <= k && k < p.k) {
@@ -129,64 +129,44 @@ snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
 template <int I>
 using IntC = std::integral_constant<int, I>;
 
-// The single-chunk layers of kShortChunks (never double-buffered).
-template <int V, typename F>
-snn_status short_variant(const Plan& p, F&& f) {
-    switch (p.k) {
+template <int IO, int V, typename F>
+snn_status chunk_variant(const Plan& p, F&& f) {
+    constexpr int K = chunk_steps(V == 8 ? 4 : V);
+    if (p.pipe) {
+        if (p.k != K) return SNN_E_UNSUPPORTED;   // no plan pairs another chunk with these lanes
+        return f(IntC<V>{}, IntC<K>{}, std::true_type{});
+    }
+    if (p.k == K) return f(IntC<V>{}, IntC<K>{}, std::false_type{});
+    switch (p.k) {   // the single-chunk layers of kShortChunks
         case 4: return f(IntC<V>{}, IntC<4>{}, std::false_type{});
         case 8: return f(IntC<V>{}, IntC<8>{}, std::false_type{});
-        default: return f(IntC<V>{}, IntC<16>{}, std::false_type{});
+        case 16: return f(IntC<V>{}, IntC<16>{}, std::false_type{});
+        default: return SNN_E_UNSUPPORTED;
     }
 }
 
+// Lane widths: fp32 2 or 1; bf16 4, 2 or 1, and 8 in the forward.
 template <int IO, typename F>
 snn_status forward_variant(const Plan& p, F&& f) {
-    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
-    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
-    if (!p.pipe && p.k < chunk_steps(IO, p.vb, false)) {
-        switch (p.vf) {
-            case 8: if constexpr (IO == SNN_IO_BF16) return short_variant<8>(p, f); else break;
-            case 4: return short_variant<4>(p, f);
-            case 2: return short_variant<2>(p, f);
-            default: return short_variant<1>(p, f);
-        }
+    switch (p.vf) {
+        case 8: if constexpr (IO == SNN_IO_BF16) return chunk_variant<IO, 8>(p, f); break;
+        case 4: if constexpr (IO == SNN_IO_BF16) return chunk_variant<IO, 4>(p, f); break;
+        case 2: return chunk_variant<IO, 2>(p, f);
+        case 1: return chunk_variant<IO, 1>(p, f);
     }
-    if constexpr (IO == SNN_IO_BF16) {
-        if (p.vf == 8)   // 8-wide lanes keep the chunk of the 4-wide backward they pair with
-            return p.pipe ? f(IntC<8>{}, IntC<K4p>{}, std::true_type{}) : f(IntC<8>{}, IntC<K4>{}, std::false_type{});
-    }
-    switch (p.vf * 2 + int(p.pipe)) {
-        case 8: return f(IntC<4>{}, IntC<K4>{}, std::false_type{});
-        case 9: return f(IntC<4>{}, IntC<K4p>{}, std::true_type{});
-        case 4: return f(IntC<2>{}, IntC<K2>{}, std::false_type{});
-        case 5: return f(IntC<2>{}, IntC<K2>{}, std::true_type{});
-        case 2: return f(IntC<1>{}, IntC<K1>{}, std::false_type{});
-        default: return f(IntC<1>{}, IntC<K1>{}, std::true_type{});
-    }
+    return SNN_E_UNSUPPORTED;
 }
 
 template <int IO, typename F>
 snn_status backward_variant(const Plan& p, F&& f) {
-    constexpr int K4 = chunk_steps(IO, 4, false), K4p = chunk_steps(IO, 4, true);
-    constexpr int K2 = chunk_steps(IO, 2, false), K1 = chunk_steps(IO, 1, false);
-    if (!p.pipe && p.k < chunk_steps(IO, p.vb, false)) {
-        switch (p.vb) {
-            case 4: return short_variant<4>(p, f);
-            case 2: return short_variant<2>(p, f);
-            default: return short_variant<1>(p, f);
-        }
+    switch (p.vb) {
+        case 4: if constexpr (IO == SNN_IO_BF16) return chunk_variant<IO, 4>(p, f); break;
+        case 2: return chunk_variant<IO, 2>(p, f);
+        case 1: return chunk_variant<IO, 1>(p, f);
     }
-    switch (p.vb * 2 + int(p.pipe)) {
-        case 8: return f(IntC<4>{}, IntC<K4>{}, std::false_type{});
-        case 9: return f(IntC<4>{}, IntC<K4p>{}, std::true_type{});
-        case 4: return f(IntC<2>{}, IntC<K2>{}, std::false_type{});
-        case 5: return f(IntC<2>{}, IntC<K2>{}, std::true_type{});
-        case 2: return f(IntC<1>{}, IntC<K1>{}, std::false_type{});
-        default: return f(IntC<1>{}, IntC<K1>{}, std::true_type{});
-    }
+    return SNN_E_UNSUPPORTED;
 }
 
-// Launchers, one per kernel translation unit (defined by explicit instantiation there).
 // v_in / v_last / g_in / g_out: the segment state of a sequence split along time (each may
 // be null; see snn_lif_forward_seg and snn_lif_backward_seg).
 template <int IO, int SPK>

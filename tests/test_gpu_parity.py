@@ -215,21 +215,23 @@ def test_gain_glue(H, io, spk, T, B, F):
     assert np.all(np.abs(H.to_host_f32(gs) - ref) <= rtol * bound)
 
 
-# Shapes that reach every lane/chunk plan of the library (lanes per neuron group V in
-# {4, 2, 1}, single or multi-chunk, double-buffered or not, with a short tail chunk), run
-# in full on the GPU and checked on sampled neuron columns.
+# Shapes that reach every lane/chunk plan of the library, run in full on the GPU and checked
+# on sampled neuron columns.  Backward lanes: fp32 2 neurons (1 when N is odd); bf16 4 on
+# layers of at least 2^20 neurons, else 2 or 1; the bf16 forward takes 8 per lane from 2^21.
+# Chunks: 16 steps (32 at 1 per lane), double-buffered below 2^20 lanes, a short tail chunk
+# when K does not divide T, and 4/8/16-step single chunks for short layers.
 PLAN_SHAPES = [
-    (16, 1 << 20),          # 4 neurons per lane, one chunk
-    (40, (1 << 20) + 4),    # 4 per lane, double-buffered 8-step chunks, tail
-    (40, 1 << 22),          # 4 per lane, 16-step chunks, tail
+    (16, 1 << 20),          # one chunk (fp32 2 per lane, bf16 4)
+    (40, (1 << 20) + 4),    # fp32 double-buffered, tail; bf16 4 per lane, 3 chunks, tail
+    (40, 1 << 22),          # multi-chunk with a tail, not double-buffered (bf16 forward 8 per lane)
     (16, 524290),           # 2 per lane, one chunk
     (40, 600002),           # 2 per lane, double-buffered, tail
     (40, 262145),           # 1 per lane (odd N), double-buffered 32-step chunks, tail
     (20, (1 << 20) + 1),    # 1 per lane, one chunk
-    (4, 1 << 20),           # short layers: one 4-step chunk, 4 per lane
+    (4, 1 << 20),           # short layers: one 4-step chunk
     (3, 1 << 21),           # 4-step chunk with a tail (bf16: 8 per lane in the forward)
     (8, 524290),            # one 8-step chunk, 2 per lane
-    (6, 1 << 22),           # 8-step chunk with a tail, 4 per lane (bf16 forward: 8)
+    (6, 1 << 22),           # 8-step chunk with a tail (bf16 forward: 8 per lane)
     (12, 262145),           # one 16-step chunk at 1 per lane (whose long chunk is 32 steps)
 ]
 
