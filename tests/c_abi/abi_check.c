@@ -1,0 +1,195 @@
+/* A plain-C client of libsnnlif: device memory from hipMalloc, a stream from
+ * hipStreamCreate, and nothing but the C ABI of include/snn_lif.h -- no Python, no torch.
+ * It runs the fused forward and backward of several layers (fp32 and bf16 I/O, u8 and bit
+ * spikes, hard and soft reset, one and several chunks, ragged N) and compares them with
+ * the CPU oracle (test infrastructure) on the same seeded inputs: spikes exactly (a
+ * mismatch is forgiven only strictly within 1e-5 of V_th, and that neuron is then left
+ * out), membranes bit for bit, dL/dx within rtol * bound (1e-5 fp32, 2e-2 bf16).  It also
+ * checks argument errors.  Exit status 0 when everything matches. */
+#include <hip/hip_runtime_api.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "lif_oracle.h"
+#include "snn_lif.h"
+
+/* the seeded input generator (synth/gen.c) */
+void synth_fill_f32(uint64_t seed, uint64_t stream, int kind, double a, double b, int64_t start, int64_t count,
+                    float *out);
+void synth_f32_to_bf16(const float *in, uint16_t *out, int64_t count);
+
+#define HIP_OK(call)                                                              \
+    do {                                                                          \
+        hipError_t e_ = (call);                                                   \
+        if (e_ != hipSuccess) {                                                   \
+            fprintf(stderr, "%s failed: %s\n", #call, hipGetErrorString(e_));     \
+            exit(3);                                                              \
+        }                                                                         \
+    } while (0)
+
+typedef struct {
+    int64_t T, N;
+    int32_t reset, io, spk;
+    float decay, v_th, v_reset, alpha;
+    uint64_t seed;
+} layer_case;
+
+static float widen_bf16(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+static void *dev_alloc(size_t bytes)
+{
+    void *p = NULL;
+    if (bytes) HIP_OK(hipMalloc(&p, bytes));
+    return p;
+}
+
+static int run_case(const layer_case *c, hipStream_t stream)
+{
+    const int64_t T = c->T, N = c->N, TN = T * N;
+    const int bf16 = c->io == SNN_IO_BF16;
+    const size_t esz = bf16 ? 2 : 4;
+    snn_lif_cfg cfg = {c->decay, c->v_th, c->v_reset, c->alpha, c->reset, c->io, c->spk};
+
+    /* inputs: x ~ N(0.5, 0.5), dL/dy ~ N(0, 1); bf16 I/O rounds them, the oracle gets the
+     * exact widened values */
+    float *x = malloc(TN * 4), *gs = malloc(TN * 4);
+    uint16_t *x16 = malloc(TN * 2), *gs16 = malloc(TN * 2);
+    synth_fill_f32(c->seed, 0, 0, 0.5, 0.5, 0, TN, x);
+    synth_fill_f32(c->seed, 1, 0, 0.0, 1.0, 0, TN, gs);
+    if (bf16) {
+        synth_f32_to_bf16(x, x16, TN);
+        synth_f32_to_bf16(gs, gs16, TN);
+        for (int64_t i = 0; i < TN; ++i) {
+            x[i] = widen_bf16(x16[i]);
+            gs[i] = widen_bf16(gs16[i]);
+        }
+    }
+
+    size_t row = 0, saved_bytes = 0;
+    if (snn_spike_row_bytes(&cfg, N, &row) != SNN_OK || snn_lif_saved_bytes(&cfg, T, N, &saved_bytes) != SNN_OK) {
+        fprintf(stderr, "size queries failed\n");
+        return 1;
+    }
+    void *dx = dev_alloc(TN * esz), *dgs = dev_alloc(TN * esz), *dgx = dev_alloc(TN * esz);
+    void *dspk = dev_alloc(T * row), *dsaved = dev_alloc(saved_bytes);
+    float *dv = dev_alloc(TN * 4);
+    HIP_OK(hipMemcpy(dx, bf16 ? (void *)x16 : (void *)x, TN * esz, hipMemcpyHostToDevice));
+    HIP_OK(hipMemcpy(dgs, bf16 ? (void *)gs16 : (void *)gs, TN * esz, hipMemcpyHostToDevice));
+
+    snn_status st = snn_lif_forward(&cfg, T, N, dx, dspk, dsaved, dv, stream);
+    if (st == SNN_OK) st = snn_lif_backward(&cfg, T, N, dx, dsaved, dgs, dgx, stream);
+    if (st != SNN_OK) {
+        fprintf(stderr, "library call failed: %s\n", snn_status_str(st));
+        return 1;
+    }
+    HIP_OK(hipStreamSynchronize(stream));
+
+    uint8_t *spk = malloc(T * row);
+    float *v = malloc(TN * 4), *gx = malloc(TN * 4);
+    uint16_t *gx16 = malloc(TN * 2);
+    HIP_OK(hipMemcpy(spk, dspk, T * row, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(v, dv, TN * 4, hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(bf16 ? (void *)gx16 : (void *)gx, dgx, TN * esz, hipMemcpyDeviceToHost));
+    if (bf16)
+        for (int64_t i = 0; i < TN; ++i) gx[i] = widen_bf16(gx16[i]);
+
+    /* the oracle on the same inputs */
+    lif_oracle_params p = {c->decay, c->v_th, c->v_reset, c->alpha, c->reset == SNN_RESET_SOFT};
+    uint8_t *y_ref = malloc(TN);
+    float *v_ref = malloc(TN * 4);
+    double *gsd = malloc(TN * 8), *gsm = malloc(TN * 8), *g_ref = malloc(TN * 8), *bound = malloc(TN * 8);
+    for (int64_t i = 0; i < TN; ++i) {
+        gsd[i] = gs[i];
+        gsm[i] = fabs((double)gs[i]);
+    }
+    lif_oracle_forward(&p, T, N, x, NULL, NULL, y_ref, v_ref);
+    lif_oracle_backward(&p, T, N, v_ref, y_ref, gsd, gsm, NULL, g_ref, bound);
+
+    const double rtol = bf16 ? 2e-2 : 1e-5;
+    int64_t hard = 0, forgiven = 0, v_bad = 0, g_bad = 0, ties = 0;
+    uint8_t *excluded = calloc(N, 1);
+    for (int64_t t = 0; t < T; ++t) {
+        for (int64_t n = 0; n < N; ++n) {
+            if (excluded[n]) continue;
+            const int64_t i = t * N + n;
+            const int y = c->spk == SNN_SPK_U8 ? spk[t * row + n] : (spk[t * row + (n >> 3)] >> (n & 7)) & 1;
+            const double dist = fabs((double)v_ref[i] - (double)c->v_th);
+            ties += v_ref[i] == c->v_th;
+            if (y != y_ref[i]) {
+                if (dist > 0 && dist < 1e-5) {
+                    ++forgiven;
+                    excluded[n] = 1;
+                    continue;
+                }
+                ++hard;
+            }
+            if (memcmp(&v[i], &v_ref[i], 4) != 0) ++v_bad;
+        }
+    }
+    for (int64_t i = 0; i < TN; ++i) {
+        if (excluded[i % N]) continue;
+        if (!(fabs((double)gx[i] - g_ref[i]) <= rtol * bound[i] + 1e-30)) ++g_bad;
+    }
+    printf("T=%lld N=%lld %s %s %s: ties=%lld forgiven=%lld hard=%lld v_unequal=%lld grad_bad=%lld\n",
+           (long long)T, (long long)N, c->reset == SNN_RESET_SOFT ? "soft" : "hard", bf16 ? "bf16" : "f32",
+           c->spk == SNN_SPK_U8 ? "u8" : "bits", (long long)ties, (long long)forgiven, (long long)hard,
+           (long long)v_bad, (long long)g_bad);
+
+    HIP_OK(hipFree(dx));
+    HIP_OK(hipFree(dgs));
+    HIP_OK(hipFree(dgx));
+    HIP_OK(hipFree(dspk));
+    if (dsaved) HIP_OK(hipFree(dsaved));
+    HIP_OK(hipFree(dv));
+    free(x), free(gs), free(x16), free(gs16), free(spk), free(v), free(gx), free(gx16);
+    free(y_ref), free(v_ref), free(gsd), free(gsm), free(g_ref), free(bound), free(excluded);
+    return (hard || v_bad || g_bad) ? 1 : 0;
+}
+
+/* argument errors come back as status codes, before anything is launched */
+static int check_errors(hipStream_t stream)
+{
+    snn_lif_cfg cfg = {0.5f, 1.0f, 0.0f, 4.0f, SNN_RESET_HARD, SNN_IO_F32, SNN_SPK_U8};
+    snn_lif_cfg bad = cfg;
+    bad.decay = 2.0f;
+    char *buf = dev_alloc(4096);
+    int fails = 0;
+    fails += snn_lif_forward(NULL, 4, 64, buf, buf, NULL, NULL, stream) != SNN_E_NULL;
+    fails += snn_lif_forward(&bad, 4, 64, buf, buf, NULL, NULL, stream) != SNN_E_PARAM;
+    fails += snn_lif_forward(&cfg, -1, 64, buf, buf, NULL, NULL, stream) != SNN_E_SHAPE;
+    fails += snn_lif_forward(&cfg, 4, 64, buf + 4, buf + 1024, NULL, NULL, stream) != SNN_E_ALIGN;
+    fails += snn_lif_backward(&cfg, 4, 64, buf, NULL, NULL, buf, stream) != SNN_E_NULL;
+    fails += snn_lif_forward(&cfg, 0, 64, NULL, NULL, NULL, NULL, stream) != SNN_OK;
+    fails += snn_status_str(SNN_E_ALIGN) == NULL;
+    HIP_OK(hipFree(buf));
+    printf("argument errors: %s\n", fails ? "FAILED" : "ok");
+    return fails ? 1 : 0;
+}
+
+int main(void)
+{
+    const layer_case cases[] = {
+        {40, 5003, SNN_RESET_HARD, SNN_IO_F32, SNN_SPK_U8, 0.5f, 1.0f, 0.0f, 4.0f, 11},
+        {33, 65536, SNN_RESET_HARD, SNN_IO_F32, SNN_SPK_BITS, 0.2f, 0.3f, 0.0f, 4.0f, 12},
+        {20, 4096, SNN_RESET_SOFT, SNN_IO_BF16, SNN_SPK_BITS, 0.75f, 1.0f, 0.0f, 4.0f, 13},
+        {4, 1 << 20, SNN_RESET_HARD, SNN_IO_BF16, SNN_SPK_U8, 0.5f, 1.0f, 0.25f, 2.0f, 14},
+        {48, 3 << 18, SNN_RESET_SOFT, SNN_IO_F32, SNN_SPK_U8, 0.75f, 1.0f, 0.0f, 4.0f, 15},
+    };
+    hipStream_t stream;
+    HIP_OK(hipStreamCreate(&stream));
+    int fails = check_errors(stream);
+    for (size_t i = 0; i < sizeof cases / sizeof cases[0]; ++i) fails += run_case(&cases[i], stream);
+    HIP_OK(hipStreamDestroy(stream));
+    printf("%s\n", fails ? "FAILED" : "all cases match the oracle");
+    return fails ? 1 : 0;
+}

@@ -151,3 +151,16 @@ def test_empty_problems_are_noops(nat):
     nat.snn_lif_backward(cfg, 8, 0, None, None, None, None, 0)
     nat.snn_gain_spikes_forward(cfg, 8, 0, 32, None, None, None, 0)
     nat.snn_gain_grad_backward(cfg, 0, 2, 32, None, None, None, 0)
+
+
+def test_c_client_links():
+    """The plain-C client builds against the header and links the library, the oracle, the
+    generator and the HIP runtime (running it needs the GPU)."""
+    import subprocess
+
+    from tests import c_abi
+    c_abi.build()
+    out = subprocess.run(["ldd", c_abi.BIN], capture_output=True, text=True).stdout
+    assert "not found" not in out
+    for lib in ("libsnnlif.so", "liboracle.so", "libsynth.so", "libamdhip64"):
+        assert lib in out, lib
