@@ -79,17 +79,35 @@ def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None, gy_mag=Non
     p = oracle.Params.of(w.params)
     y_ref, v_ref = oracle.forward(p, x_np)
     gx_ref, bound = oracle.backward(p, v_ref, y_ref, gs_np, gy_mag)
-    y_gpu = parity.unpack_spikes(to_host_f32(spikes) if w.spk == "io" else spikes.cpu().numpy(), w.N, w.spk)
-    v_gpu = None if v is None else v.cpu().numpy()
-    g_gpu = to_host_f32(gx)
-    if cols is not None:
-        y_gpu = y_gpu[:, cols]
-        v_gpu = None if v_gpu is None else v_gpu[:, cols]
-        g_gpu = g_gpu[:, cols]
+    if cols is not None and w.T * w.N > (1 << 31):
+        # a layer too large to copy whole: gather the sampled columns on the device
+        y_gpu, v_gpu, g_gpu = gather_columns(w, spikes, v, gx, cols)
+    else:
+        y_gpu = parity.unpack_spikes(to_host_f32(spikes) if w.spk == "io" else spikes.cpu().numpy(), w.N, w.spk)
+        v_gpu = None if v is None else v.cpu().numpy()
+        g_gpu = to_host_f32(gx)
+        if cols is not None:
+            y_gpu = y_gpu[:, cols]
+            v_gpu = None if v_gpu is None else v_gpu[:, cols]
+            g_gpu = g_gpu[:, cols]
     rep = parity.compare_forward(y_gpu, y_ref, v_ref, w.params.v_th, v_gpu=v_gpu, rep=rep)
     rtol = parity.RTOL_BF16 if w.io == "bf16" else parity.RTOL_F32
     parity.compare_grad(g_gpu, gx_ref, bound, rtol, rep)
     return rep, (y_ref, v_ref, gx_ref, bound)
+
+
+def gather_columns(w: W.Workload, spikes, v, gx, cols: np.ndarray):
+    """Spikes (0/1), membranes and dL/dx of neuron columns `cols`, gathered on the device."""
+    c = torch.from_numpy(np.asarray(cols, dtype=np.int64)).to(DEV)
+    if w.spk == "io":
+        y = to_host_f32(spikes.index_select(1, c)).astype(np.uint8)
+    elif w.spk == "u8":
+        y = spikes.index_select(1, c).cpu().numpy()
+    else:
+        byte = spikes.index_select(1, c >> 3).to(torch.int32)
+        y = ((byte >> (c & 7).to(torch.int32)) & 1).to(torch.uint8).cpu().numpy()
+    vv = None if v is None else v.index_select(1, c).cpu().numpy()
+    return y, vv, to_host_f32(gx.index_select(1, c))
 
 
 def check_full(w: W.Workload, *, v_out=True, inplace=False):
@@ -117,5 +135,5 @@ def synth_bf16(a: np.ndarray) -> np.ndarray:
 
 
 __all__ = ["DEV", "say", "cfg_of", "to_dev", "to_host_f32", "upload_rows", "sample_columns", "gpu_layer",
-           "compare_layer", "check_full", "check_sampled", "synth_bf16", "layer", "native", "np", "torch", "W",
+           "compare_layer", "gather_columns", "check_full", "check_sampled", "synth_bf16", "layer", "native", "np", "torch", "W",
            "oracle", "parity"]

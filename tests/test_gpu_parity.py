@@ -29,6 +29,8 @@ PARAMS = {
     "rest": dict(decay=0.75, v_th=1.0, v_reset=0.25, alpha=2.0),
     "k1": dict(decay=1.0, v_th=1.0),
     "k0": dict(decay=0.0, v_th=0.5),
+    "neg_th": dict(decay=0.5, v_th=-0.25),              # a negative threshold
+    "rest_above": dict(decay=0.9, v_th=0.5, v_reset=0.75),  # reset value above the threshold
 }
 COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits", "io"]))
 
@@ -156,6 +158,18 @@ def test_workload_large(H, T):
     w = H.W.WORKLOADS["large"].with_T(T)
     rep = H.check_sampled(w, 1 << 20 if T == 256 else 1 << 16)
     H.say(f"large T={T}: {rep}")
+    assert rep.ok(), str(rep)
+    H.torch.cuda.empty_cache()
+
+
+def test_max_neurons(H):
+    """The largest layer the ABI accepts in one row: N = 2^31 - 1 (odd, so one neuron per
+    lane: a grid of 2^31 lanes), three steps (a short chunk with a tail); sampled columns
+    include both ends."""
+    N = (1 << 31) - 1
+    w = H.W.custom("maxN", 3, N, H.W.HARD_05, seed=31, x_dist=("normal", 0.6, 0.5))
+    rep = H.check_sampled(w, 1 << 12)
+    H.say(f"max N: {rep}")
     assert rep.ok(), str(rep)
     H.torch.cuda.empty_cache()
 
