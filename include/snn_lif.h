@@ -41,7 +41,7 @@ typedef enum {
     SNN_E_SHAPE = -2,       /* negative or too large T, N, B, F */
     SNN_E_PARAM = -3,       /* a hyper-parameter or enum value out of range */
     SNN_E_ALIGN = -4,       /* a data pointer is not 16-byte aligned */
-    SNN_E_UNSUPPORTED = -5, /* a combination this build does not implement */
+    SNN_E_UNSUPPORTED = -5, /* a combination the library does not implement */
     SNN_E_LAUNCH = -6       /* the HIP runtime rejected the kernel launch */
 } snn_status;
 
