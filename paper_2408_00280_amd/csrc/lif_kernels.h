@@ -5,8 +5,8 @@
 // Design (see the header for the operation itself):
 //  * Neurons are independent (Sec. 3.1), so each lane owns V consecutive neurons and walks
 //    all T steps with their membranes in VGPRs (temporal fusion, Sec. 3.2).  Rows of the
-//    time-major [T][N] tensors are read and written coalesced along N, 16 bytes per lane
-//    (V = 4 fp32 or V = 8 bf16 neurons) when N is a multiple of V; otherwise V = 1.
+//    time-major [T][N] tensors are read and written coalesced along N, 8 or 16 bytes per
+//    lane (V = 2 fp32, V = 4 or 8 bf16 neurons) when N is a multiple of V; otherwise fewer.
 //  * Time is processed in chunks of K steps.  All K input rows of a chunk are loaded before
 //    the first step of the chunk is computed (they do not depend on the recurrence), so
 //    every lane keeps K loads in flight.
