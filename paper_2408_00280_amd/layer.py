@@ -33,6 +33,11 @@ class LifConfig:
         return IO_DTYPES[self.io]
 
 
+def _require(ok: bool, what: str):
+    if not ok:
+        raise ValueError(what)
+
+
 def _TN(x: torch.Tensor):
     T = x.shape[0]
     return T, (x.numel() // T if T else 0)
@@ -56,7 +61,7 @@ def forward(cfg: LifConfig, x: torch.Tensor, *, v_out: bool = False, out=None, v
             stream=None):
     """Fused forward of x[T, ...] (cfg.dtype, contiguous).  Returns (spikes, saved, v_or_None).
     v_in / v_last ([N] float32): segment state of a sequence split along time."""
-    assert x.dtype == cfg.dtype and x.is_contiguous()
+    _require(x.dtype == cfg.dtype and x.is_contiguous(), f"x must be a contiguous {cfg.dtype} tensor")
     T, N = _TN(x)
     spikes, saved, v = out if out is not None else alloc_forward(cfg, T, N, x.device, v_out)
     sv = saved if saved.numel() else None
@@ -71,7 +76,8 @@ def backward(cfg: LifConfig, x: torch.Tensor, saved: torch.Tensor, grad_s: torch
              grad_x: torch.Tensor | None = None, v_in=None, g_in=None, g_out=None, stream=None) -> torch.Tensor:
     """Fused backward; returns dL/dx with x's shape and dtype (in place if grad_x is grad_s).
     v_in / g_in / g_out ([N] float32): segment state of a sequence split along time."""
-    assert grad_s.dtype == cfg.dtype and grad_s.shape == x.shape and grad_s.is_contiguous()
+    _require(grad_s.dtype == cfg.dtype and grad_s.shape == x.shape and grad_s.is_contiguous(),
+             f"grad_s must be a contiguous {cfg.dtype} tensor shaped like x")
     T, N = _TN(x)
     if grad_x is None:
         grad_x = torch.empty_like(grad_s)
@@ -101,7 +107,8 @@ def backward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, s
     """Backward of forward_gain; returns dL/d spikes_in = gain[f] * dL/dx, [T][N] in cfg's I/O
     dtype (in place if grad_s_in is grad_s)."""
     T = spikes_in.shape[0]
-    assert grad_s.dtype == cfg.dtype and tuple(grad_s.shape) == (T, B * F) and grad_s.is_contiguous()
+    _require(grad_s.dtype == cfg.dtype and tuple(grad_s.shape) == (T, B * F) and grad_s.is_contiguous(),
+             f"grad_s must be a contiguous {cfg.dtype} tensor of shape ({T}, {B * F})")
     if grad_s_in is None:
         grad_s_in = torch.empty_like(grad_s)
     native.snn_lif_backward_gain(cfg.c(), T, B, F, spikes_in, gain, saved if saved.numel() else None, grad_s,

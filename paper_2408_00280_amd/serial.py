@@ -13,7 +13,8 @@ from . import layer, native
 
 def forward(cfg: layer.LifConfig, x: torch.Tensor, *, stream=None):
     """x[T][N] -> (spikes in cfg.spk format, v[T][N] fp32 membranes kept for the backward)."""
-    assert x.dtype == cfg.dtype and x.is_contiguous()
+    if x.dtype != cfg.dtype or not x.is_contiguous():
+        raise ValueError(f"x must be a contiguous {cfg.dtype} tensor")
     T = x.shape[0]
     N = x.numel() // T if T else 0
     spikes, _, _ = layer.alloc_forward(cfg, T, N, x.device)
