@@ -150,8 +150,8 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, 
  * nn.Sequential); fusing that operator into the layer goes beyond the paper and is
  * offered for the per-feature gain above only.  Same shapes as the gain functions
  * (N = B*F, neuron (b, f) at b*F + f); everything else as snn_lif_forward / backward.
- *   spikes_in  previous layer's spikes, in THIS cfg's spike format, which must be
- *              SNN_SPK_U8 or SNN_SPK_BITS (SNN_E_UNSUPPORTED otherwise).
+ *   spikes_in  previous layer's spikes, in THIS cfg's spike format (u8, bits, or 0/1
+ *              values of the I/O dtype shaped [T][N] as the autograd path passes them).
  *   gain       device float32 [F].  The input current uses gain[f] rounded to cfg->io,
  *              so the layer's spikes, membranes and checkpoints equal, bit for bit, those
  *              of snn_gain_spikes_forward followed by snn_lif_forward.
@@ -162,7 +162,8 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, 
  *              unfused pair rounds dL/dx first, so bf16 results may differ there in the
  *              last bit).  grad_s_in may be the same buffer as grad_s; no other overlap.
  * x is never materialised: per (t, n) the forward reads 1 B (u8) or 1/8 B (bits) of input
- * instead of 4 B or 2 B. */
+ * instead of 4 B or 2 B (with I/O-dtype spikes it saves the glue kernel's write and read of
+ * x). */
 snn_status snn_lif_forward_gain(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
                                 const void *spikes_in, const float *gain, void *spikes,
                                 void *saved, float *v_out, void *stream);

@@ -61,3 +61,56 @@ class LIFLayer(torch.nn.Module):
     def extra_repr(self) -> str:
         return (f"decay={self.decay}, v_th={self.v_th}, v_reset={self.v_reset}, alpha={self.alpha}, "
                 f"reset={self.reset}")
+
+
+class FusedGainLIF(torch.autograd.Function):
+    """A LIF layer fed by the previous layer's spikes through a fixed per-feature gain:
+    input current gain[f] * spikes_in[t, ..., f], formed inside the fused kernels.  The
+    backward returns dL/d spikes_in = gain[f] * dL/dx; the gain gets no gradient."""
+
+    @staticmethod
+    def forward(ctx, spikes_in: torch.Tensor, gain: torch.Tensor, cfg: layer.LifConfig):
+        if spikes_in.dtype not in _IO or cfg.io != _IO[spikes_in.dtype] or cfg.spk != "io":
+            raise TypeError("FusedGainLIF takes float32/bfloat16 spikes and a cfg with io matching them and spk='io'")
+        F = gain.numel()
+        if spikes_in.shape[-1] != F or gain.dtype != torch.float32:
+            raise ValueError("gain must be float32 with one entry per feature (the last axis of spikes_in)")
+        s = spikes_in.contiguous()
+        T = s.shape[0]
+        B = s.numel() // (T * F) if T else 0
+        s2 = s.view(T, B * F)
+        g = gain.contiguous()
+        spikes, saved, _ = layer.forward_gain(cfg, s2, g, B, F)
+        ctx.save_for_backward(s2, g, saved)
+        ctx.cfg, ctx.shape, ctx.BF = cfg, spikes_in.shape, (B, F)
+        return spikes.view(spikes_in.shape)
+
+    @staticmethod
+    def backward(ctx, grad_y: torch.Tensor):
+        s2, g, saved = ctx.saved_tensors
+        B, F = ctx.BF
+        gy = grad_y.to(s2.dtype).contiguous().view(s2.shape)
+        grad_in = layer.backward_gain(ctx.cfg, s2, g, saved, gy, B, F)
+        return grad_in.view(ctx.shape), None, None
+
+
+class GainLIF(torch.nn.Module):
+    """LIF neurons fed by spikes through a fixed per-feature gain (the feature axis is the
+    last one): the fused form of ``x = gain * spikes`` followed by a :class:`LIFLayer`, with
+    the same spikes and membranes and without storing x."""
+
+    def __init__(self, gain: torch.Tensor, decay: float, v_th: float, v_reset: float = 0.0, alpha: float = 4.0,
+                 reset: str = "hard"):
+        super().__init__()
+        self.register_buffer("gain", gain.detach().to(torch.float32).contiguous())
+        self.decay, self.v_th, self.v_reset, self.alpha, self.reset = decay, v_th, v_reset, alpha, reset
+
+    def cfg(self, dtype: torch.dtype) -> layer.LifConfig:
+        return layer.LifConfig(self.decay, self.v_th, self.v_reset, self.alpha, self.reset, _IO[dtype], "io")
+
+    def forward(self, spikes_in: torch.Tensor) -> torch.Tensor:
+        return FusedGainLIF.apply(spikes_in, self.gain, self.cfg(spikes_in.dtype))
+
+    def extra_repr(self) -> str:
+        return (f"features={self.gain.numel()}, decay={self.decay}, v_th={self.v_th}, v_reset={self.v_reset}, "
+                f"alpha={self.alpha}, reset={self.reset}")

@@ -30,10 +30,10 @@ UNITS = (
     [(f"fwd_io{io}_spk{spk}", "lif_forward.hip", [f"-DSNNLIF_IO={io}", f"-DSNNLIF_SPK={spk}"])
      for io in (0, 1) for spk in (0, 1, 2)]
     + [(f"fwdgain_io{io}_spk{spk}", "lif_forward.hip", [f"-DSNNLIF_IO={io}", f"-DSNNLIF_SPK={spk}", "-DSNNLIF_GAIN=1"])
-       for io in (0, 1) for spk in (0, 1)]
+       for io in (0, 1) for spk in (0, 1, 2)]
     + [(f"bwd_io{io}", "lif_backward.hip", [f"-DSNNLIF_IO={io}"]) for io in (0, 1)]
     + [(f"bwdgain_io{io}_spk{spk}", "lif_backward.hip", [f"-DSNNLIF_IO={io}", f"-DSNNLIF_SPK={spk}", "-DSNNLIF_GAIN=1"])
-       for io in (0, 1) for spk in (0, 1)]
+       for io in (0, 1) for spk in (0, 1, 2)]
     + [("glue", "lif_glue.hip", []), ("serial", "lif_serial.hip", []), ("api", "snn_lif_api.hip", [])]
 )
 

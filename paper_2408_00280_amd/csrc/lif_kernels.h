@@ -340,8 +340,9 @@ __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
 // Where the input current comes from is a policy:
 //   DenseIn     -- x[T][N] in the I/O dtype (a layer fed by an ANN operator);
 //   GainSpikeIn -- x[t][b][f] = gain[f] * spikes_in[t][b][f], read straight from the previous
-//                  layer's spikes (a stack fused across its per-feature gain; the gain is
-//                  rounded to the I/O dtype first, as a stored input current would be).
+//                  layer's spikes in any of the spike formats (a stack fused across its
+//                  per-feature gain; the gain is rounded to the I/O dtype first, as a stored
+//                  input current would be).
 template <int IO, int V>
 struct DenseIn {
     using raw = typename IoVec<IO, V>::raw;
@@ -352,7 +353,9 @@ struct DenseIn {
 
 template <int IO, int SPK, int V>
 struct GainSpikeIn {
-    using raw = std::conditional_t<SPK == SNN_SPK_U8 && V == 8, uint64_t, uint32_t>;
+    // u8: V bytes; bits: the byte holding the lane's bits; io: V values of the I/O dtype
+    using raw = std::conditional_t<SPK == SNN_SPK_IO, typename IoVec<IO, V>::raw,
+                                   std::conditional_t<SPK == SNN_SPK_U8 && V == 8, uint64_t, uint32_t>>;
     const uint8_t* s;
     int64_t row_bytes;
     float gx[V];   // gain of the lane's neurons, rounded to the I/O dtype (forward input)
@@ -364,17 +367,26 @@ struct GainSpikeIn {
             gx[j] = IO == SNN_IO_BF16 ? bf16_lo(pack_bf16x2(gy[j], 0.0f)) : gy[j];
         }
     }
-    __device__ raw load(int64_t, int64_t t, int64_t n0) const {
-        const uint8_t* row = s + t * row_bytes;
-        if constexpr (SPK == SNN_SPK_BITS) return row[n0 >> 3];
-        else if constexpr (V == 8) return *reinterpret_cast<const uint64_t*>(row + n0);
-        else if constexpr (V == 4) return *reinterpret_cast<const uint32_t*>(row + n0);
-        else if constexpr (V == 2) return *reinterpret_cast<const uint16_t*>(row + n0);
-        else return row[n0];
+    __device__ raw load(int64_t N, int64_t t, int64_t n0) const {
+        if constexpr (SPK == SNN_SPK_IO) {
+            return IoVec<IO, V>::load(s, t * N + n0);
+        } else {
+            const uint8_t* row = s + t * row_bytes;
+            if constexpr (SPK == SNN_SPK_BITS) return row[n0 >> 3];
+            else if constexpr (V == 8) return *reinterpret_cast<const uint64_t*>(row + n0);
+            else if constexpr (V == 4) return *reinterpret_cast<const uint32_t*>(row + n0);
+            else if constexpr (V == 2) return *reinterpret_cast<const uint16_t*>(row + n0);
+            else return row[n0];
+        }
     }
     __device__ float get(const raw& r, int j, int64_t n0) const {
-        const uint32_t bit = SPK == SNN_SPK_BITS ? uint32_t(r >> ((n0 + j) & 7)) & 1u : uint32_t(r >> (8 * j)) & 1u;
-        return gx[j] * float(bit);
+        if constexpr (SPK == SNN_SPK_IO) {
+            return gx[j] * IoVec<IO, V>::get(r, j);   // spikes are 0 or 1: exact
+        } else {
+            const uint32_t bit =
+                SPK == SNN_SPK_BITS ? uint32_t(r >> ((n0 + j) & 7)) & 1u : uint32_t(r >> (8 * j)) & 1u;
+            return gx[j] * float(bit);
+        }
     }
 };
 

@@ -149,7 +149,6 @@ snn_status snn_lif_forward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, in
     snn_status st = check_cfg(cfg);
     if (st != SNN_OK) return st;
     if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
-    if (cfg->spk != SNN_SPK_U8 && cfg->spk != SNN_SPK_BITS) return SNN_E_UNSUPPORTED;
     const int64_t N = B * F;
     if (T == 0 || N == 0) return SNN_OK;
     const Plan p = make_plan(cfg, T, N);
@@ -163,13 +162,20 @@ snn_status snn_lif_forward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, in
     hipStream_t s = static_cast<hipStream_t>(stream);
     void* sv = need_saved ? saved : nullptr;
     const int r = cfg->reset;
-    if (cfg->io == SNN_IO_F32)
-        return cfg->spk == SNN_SPK_U8
-                   ? forward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s)
-                   : forward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
-    return cfg->spk == SNN_SPK_U8
-               ? forward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s)
-               : forward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+    switch (cfg->io * 4 + cfg->spk) {
+        case SNN_IO_F32 * 4 + SNN_SPK_U8:
+            return forward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_BITS:
+            return forward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_IO:
+            return forward_gain_entry<SNN_IO_F32, SNN_SPK_IO>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_U8:
+            return forward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_BITS:
+            return forward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+        default:
+            return forward_gain_entry<SNN_IO_BF16, SNN_SPK_IO>(r, p, k, T, N, F, spikes_in, gain, spikes, sv, v_out, s);
+    }
 }
 
 snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, int64_t F, const void* spikes_in,
@@ -178,7 +184,6 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, i
     snn_status st = check_cfg(cfg);
     if (st != SNN_OK) return st;
     if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
-    if (cfg->spk != SNN_SPK_U8 && cfg->spk != SNN_SPK_BITS) return SNN_E_UNSUPPORTED;
     const int64_t N = B * F;
     if (T == 0 || N == 0) return SNN_OK;
     const Plan p = make_plan(cfg, T, N);
@@ -193,13 +198,20 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, i
     hipStream_t s = static_cast<hipStream_t>(stream);
     const void* sv = need_saved ? saved : nullptr;
     const int r = cfg->reset;
-    if (cfg->io == SNN_IO_F32)
-        return cfg->spk == SNN_SPK_U8
-                   ? backward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s)
-                   : backward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
-    return cfg->spk == SNN_SPK_U8
-               ? backward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s)
-               : backward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+    switch (cfg->io * 4 + cfg->spk) {
+        case SNN_IO_F32 * 4 + SNN_SPK_U8:
+            return backward_gain_entry<SNN_IO_F32, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_BITS:
+            return backward_gain_entry<SNN_IO_F32, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_IO:
+            return backward_gain_entry<SNN_IO_F32, SNN_SPK_IO>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_U8:
+            return backward_gain_entry<SNN_IO_BF16, SNN_SPK_U8>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_BITS:
+            return backward_gain_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+        default:
+            return backward_gain_entry<SNN_IO_BF16, SNN_SPK_IO>(r, p, k, T, N, F, spikes_in, gain, sv, grad_s, grad_s_in, s);
+    }
 }
 
 snn_status snn_lif_serial_forward_step(const snn_lif_cfg* cfg, int64_t N, const void* x_t, const float* v_prev,

@@ -76,3 +76,46 @@ def test_inside_sequential(H):
     out.sum().backward()
     assert out.shape == (16, 4, 10)
     assert all(p.grad is not None and torch.isfinite(p.grad).all() for p in model.parameters())
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fused_stack_autograd(H, dtype):
+    """LIFLayer -> GainLIF(gain_12) -> GainLIF(gain_23): three layers, the later two fed
+    straight from spikes; the last layer's spikes and x.grad from torch's autograd against
+    the oracle run layer by layer (the gain rounded to the I/O dtype, as the kernels do)."""
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import GainLIF, LIFLayer
+    T, B, F = 24, 6, 1000
+    p = H.W.LifParams(0.5, 1.0)
+    w = H.W.custom("fstack", T, B * F, p, seed=43, io=dtype, spk="io", x_dist=("normal", 0.4, 0.6))
+    x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+    rng = np.random.default_rng(7)
+    gains = [rng.uniform(0.5, 2.0, size=F).astype(np.float32) for _ in range(2)]
+    x = H.to_dev(x_np, dtype).view(T, B, F).requires_grad_(True)
+    model = torch.nn.Sequential(LIFLayer(p.decay, p.v_th),
+                                GainLIF(torch.from_numpy(gains[0]), p.decay, p.v_th),
+                                GainLIF(torch.from_numpy(gains[1]), p.decay, p.v_th)).to(H.DEV)
+    y = model(x)
+    (y * H.to_dev(gs_np, dtype).view(T, B, F)).sum().backward()
+    torch.cuda.synchronize()
+
+    def rnd(a):
+        return H.parity.bf16_to_f32(H.synth_bf16(a)) if dtype == "bf16" else a
+    P = H.oracle.Params.of(p)
+    xs, ys, vs = [x_np], [], []
+    for l in range(3):
+        yl, vl = H.oracle.forward(P, xs[l])
+        ys.append(yl)
+        vs.append(vl)
+        if l < 2:
+            xs.append(rnd(H.oracle.gain_forward(yl, gains[l], B, F)))
+    gy, gym = gs_np.astype(np.float64), np.abs(gs_np.astype(np.float64))
+    for l in range(2, -1, -1):
+        gx, gm = H.oracle.backward(P, vs[l], ys[l], gy, gym)
+        if l > 0:
+            gy, gym = H.oracle.gain_backward(gx, gm, gains[l - 1], B, F)
+    rep = H.parity.compare_forward(H.to_host_f32(y.detach()).reshape(T, -1).astype(np.uint8), ys[2], vs[2], p.v_th)
+    rtol = H.parity.RTOL_BF16 if dtype == "bf16" else H.parity.RTOL_F32
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), gx, gm, rtol, rep)
+    H.say(f"fused stack autograd {dtype}: {rep}")
+    assert rep.ok(), str(rep)

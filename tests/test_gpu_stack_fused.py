@@ -21,7 +21,7 @@ def H():
     return gpu_harness
 
 
-COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits"]))
+COMBOS = list(itertools.product(["hard", "soft"], ["f32", "bf16"], ["u8", "bits", "io"]))
 
 
 def _pack(y: np.ndarray, spk: str) -> np.ndarray:
@@ -71,7 +71,8 @@ def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
     cfg = H.layer.LifConfig(0.5, 1.0, reset=reset, io=io, spk=spk)
     y_in, gain, gs = _inputs(T, B, F, io, seed)
     gs = _round_io(H, gs, io)
-    s_in = torch.from_numpy(_pack(y_in, spk)).to(H.DEV)
+    s_in = (H.to_dev(y_in.astype(np.float32), io) if spk == "io"
+            else torch.from_numpy(_pack(y_in, spk)).to(H.DEV))
     g_dev = torch.from_numpy(gain).to(H.DEV)
     gs_dev = H.to_dev(gs, io)
 
@@ -90,7 +91,7 @@ def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
 
     cols = None if n_sample is None else H.sample_columns(N, n_sample, seed=seed)
     y_ref, v_ref, gy_ref, gy_bound = _oracle_layer(H, cfg, y_in, gain, gs, io, cols)
-    y_gpu = H.parity.unpack_spikes(spikes.cpu().numpy(), N, spk)
+    y_gpu = H.parity.unpack_spikes(H.to_host_f32(spikes) if spk == "io" else spikes.cpu().numpy(), N, spk)
     v_gpu, g_gpu = v.cpu().numpy(), H.to_host_f32(g_in)
     if cols is not None:
         y_gpu, v_gpu, g_gpu = y_gpu[:, cols], v_gpu[:, cols], g_gpu[:, cols]
@@ -148,12 +149,9 @@ def test_gain_layer_errors(H):
     gain = torch.ones(F, dtype=torch.float32, device=H.DEV)
     spikes = torch.empty_like(s_in)
     gs = torch.zeros((T, B * F), dtype=torch.float32, device=H.DEV)
-    with pytest.raises(nat.SnnError) as e:   # spikes in the I/O dtype are not a fused input
-        nat.snn_lif_forward_gain(H.layer.LifConfig(0.5, 1.0, spk="io").c(), T, B, F, gs, gain, gs, None)
-    assert e.value.status == -5
     with pytest.raises(nat.SnnError) as e:
-        nat.snn_lif_backward_gain(H.layer.LifConfig(0.5, 1.0, spk="io").c(), T, B, F, gs, gain, None, gs, gs)
-    assert e.value.status == -5
+        nat.snn_lif_forward_gain(H.layer.LifConfig(1.5, 1.0).c(), T, B, F, s_in, gain, spikes, None)
+    assert e.value.status == -3
     with pytest.raises(nat.SnnError) as e:
         nat.snn_lif_forward_gain(good.c(), T, B, F, s_in, None, spikes, None)
     assert e.value.status == -1
@@ -173,7 +171,7 @@ def test_gain_layer_errors(H):
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("spk", ["u8", "bits"])
+@pytest.mark.parametrize("spk", ["u8", "bits", "io"])
 def test_workload_stack_fused(H, spk):
     """The three-layer stack workload through the fused schedule: every layer's spikes and
     membranes, dL/dx of layer 0 and dL/dy of layers 0 and 1 against the oracle's stack."""
@@ -195,7 +193,9 @@ def test_workload_stack_fused(H, spk):
     gxs, gms = H.oracle.stack_backward(p, ys, vs, gs_np, gains_np, B, F)
     rep = H.parity.Report()
     for l in range(w.layers):
-        r = H.parity.compare_forward(H.parity.unpack_spikes(states[l].spikes.cpu().numpy(), w.N, spk),
+        sp = states[l].spikes
+        r = H.parity.compare_forward(H.parity.unpack_spikes(H.to_host_f32(sp) if spk == "io" else sp.cpu().numpy(),
+                                                            w.N, spk),
                                      ys[l], vs[l], w.params.v_th, v_gpu=states[l].v.cpu().numpy())
         H.say(f"fused stack layer {l} ({spk}): rate {ys[l].mean():.3f} {r}")
         assert r.ok(), f"layer {l}: {r}"
