@@ -28,9 +28,10 @@ snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
-            return v_out ? launch(lif_forward_kernel<IO, SPK, R, Vc, Kc, true, Pc>, g, s, k, T, N, x, sp,
+            constexpr int FB = forward_batch(IO, Vc, Kc, Pc);
+            return v_out ? launch(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, true, Pc>, g, s, k, T, N, x, sp,
                                   p.row_bytes, sv, v_out, v_in, v_last)
-                         : launch(lif_forward_kernel<IO, SPK, R, Vc, Kc, false, Pc>, g, s, k, T, N, x, sp,
+                         : launch(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, false, Pc>, g, s, k, T, N, x, sp,
                                   p.row_bytes, sv, v_out, v_in, v_last);
         });
     };
@@ -56,9 +57,10 @@ snn_status forward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
-            return v_out ? launch(lif_forward_gain_kernel<IO, SPK, R, Vc, Kc, true, Pc>, g, s, k, T, N, F, si, gain,
+            constexpr int FB = forward_batch(IO, Vc, Kc, Pc);
+            return v_out ? launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, true, Pc>, g, s, k, T, N, F, si, gain,
                                   sp, p.row_bytes, sv, v_out)
-                         : launch(lif_forward_gain_kernel<IO, SPK, R, Vc, Kc, false, Pc>, g, s, k, T, N, F, si, gain,
+                         : launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, false, Pc>, g, s, k, T, N, F, si, gain,
                                   sp, p.row_bytes, sv, v_out);
         });
     };

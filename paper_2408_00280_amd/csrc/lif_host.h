@@ -53,8 +53,9 @@ struct Plan {
 };
 
 // Steps per chunk for v neurons per backward lane: the backward keeps K membranes per
-// neuron in VGPRs plus K rows of x and dL/dy (twice the rows when double-buffered).  A
-// forward lane of 8 (bf16) pairs with a backward lane of 4.
+// neuron in VGPRs plus K rows of x and dL/dy (twice the rows when double-buffered).  Large
+// bf16 layers (not double-buffered) take 32 steps at 2 neurons per lane instead: half the
+// checkpoint traffic, and bf16 rows take half the registers (make_plan).
 constexpr int chunk_steps(int v) { return v == 1 ? 32 : 16; }
 
 // A layer of T <= K steps is one chunk and keeps no checkpoint; it runs with the shortest
@@ -67,11 +68,14 @@ constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 
 inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
-    // fp32: 2 neurons per lane (8-byte rows; 4 per lane measured 1% slower on large
-    // layers); bf16: 4 per lane (8-byte rows) on layers that fill the chip, else 2
-    p.vb = N % 2 != 0 ? 1 : (c->io == SNN_IO_BF16 && N % 4 == 0 && N / 4 >= kFillLanes) ? 4 : 2;
+    // 2 neurons per lane (fp32 8-byte rows: 4 per lane measured 1% slower on large layers;
+    // bf16 4-byte rows with 32-step chunks: faster than 4 per lane with 16-step chunks),
+    // except bf16 layers of at most 16 steps that fill the chip: 4 per lane, 8-byte rows
+    p.vb = N % 2 != 0 ? 1 : 2;
+    if (c->io == SNN_IO_BF16 && T <= 16 && N % 4 == 0 && N / 4 >= kFillLanes) p.vb = 4;
     p.pipe = T > chunk_steps(p.vb) && N / p.vb < 4 * kFillLanes;
     p.k = chunk_steps(p.vb);
+    if (!p.pipe && c->io == SNN_IO_BF16 && p.vb == 2) p.k = 32;
     if (T <= p.k) {
         for (int k : kShortChunks) {
             if (T <= k && k < p.k) {
@@ -81,7 +85,7 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
         }
     }
     // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
-    p.vf = (c->io == SNN_IO_BF16 && p.vb == 4 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
+    p.vf = (c->io == SNN_IO_BF16 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
     p.row_bytes = spike_row_bytes(c, N);
     const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
     p.lanes = (covered + p.vf - 1) / p.vf;
@@ -123,6 +127,13 @@ snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
     return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
 }
 
+// Rows per load batch of the forward.  The forward never revisits a row, so it need not
+// hold a whole 32-step chunk (the checkpoint interval) in registers: it loads 16 rows at a
+// time and checkpoints after every second batch.
+constexpr int forward_batch(int io, int v, int k, bool pipe) {
+    return (!pipe && k > 16) ? 16 : k;
+}
+
 // Calls f(V, K, PIPE) -- std::integral_constant / bool_constant tags -- with the lane width
 // and chunk length the plan chose for the forward (vf) or the backward (vb): the
 // combinations a kernel translation unit instantiates.
@@ -131,21 +142,22 @@ using IntC = std::integral_constant<int, I>;
 
 template <int IO, int V, typename F>
 snn_status chunk_variant(const Plan& p, F&& f) {
-    constexpr int K = chunk_steps(V == 8 ? 4 : V);
+    constexpr int K = chunk_steps(V == 8 ? 2 : V);   // a double-buffered 8-wide lane would pair with 2-wide
     if (p.pipe) {
         if (p.k != K) return SNN_E_UNSUPPORTED;   // no plan pairs another chunk with these lanes
         return f(IntC<V>{}, IntC<K>{}, std::true_type{});
     }
-    if (p.k == K) return f(IntC<V>{}, IntC<K>{}, std::false_type{});
-    switch (p.k) {   // the single-chunk layers of kShortChunks
+    switch (p.k) {   // the long chunks, and the single-chunk layers of kShortChunks
         case 4: return f(IntC<V>{}, IntC<4>{}, std::false_type{});
         case 8: return f(IntC<V>{}, IntC<8>{}, std::false_type{});
         case 16: return f(IntC<V>{}, IntC<16>{}, std::false_type{});
-        default: return SNN_E_UNSUPPORTED;
+        case 32: if constexpr (V == 1 || (IO == SNN_IO_BF16 && V != 4)) return f(IntC<V>{}, IntC<32>{}, std::false_type{});
+                 break;
     }
+    return SNN_E_UNSUPPORTED;
 }
 
-// Lane widths: fp32 2 or 1; bf16 4, 2 or 1, and 8 in the forward.
+// Lane widths: 2 or 1; bf16 also 4 (short layers) and 8 (the forward of large layers).
 template <int IO, typename F>
 snn_status forward_variant(const Plan& p, F&& f) {
     switch (p.vf) {

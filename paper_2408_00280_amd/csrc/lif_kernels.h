@@ -422,14 +422,15 @@ __device__ __forceinline__ void forward_rows(const LifK& c, const In& in, const 
 }
 
 // Forward of one workgroup's lanes.  Chunks 0 .. n_full-1 have K steps; a tail chunk of
-// T % K steps follows when T % K != 0.  After every chunk but the last the membrane is
-// checkpointed to saved[chunk][N].  PIPE: double-buffered chunks -- the next chunk's rows
-// are in flight while the current chunk is computed (for layers with few lanes, where
-// occupancy alone cannot hide the memory latency).
+// T % K steps follows when T % K != 0.  The membrane is checkpointed to saved[i][N] after
+// step (i + 1) KC, for every such step before T: KC, the backward's chunk, is a multiple
+// of K, since the forward may load a long chunk in shorter batches.  PIPE: double-buffered
+// chunks -- the next chunk's rows are in flight while the current chunk is computed (for
+// layers with few lanes, where occupancy alone cannot hide the memory latency); KC == K.
 // Segment state (a sequence split along time): v_in, if not null, is the membrane the
 // previous segment ended with, and the spike state entering the first step is v_in >= V_th;
 // v_last, if not null, receives the membrane after the last step.
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE, bool ALL, typename In>
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE, bool ALL, typename In>
 __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
                                               uint8_t* __restrict__ spikes, int64_t row_bytes,
                                               float* __restrict__ saved, float* __restrict__ v_out,
@@ -459,11 +460,17 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
         if (ALL || active) load_rows<In, K, true, false>(in, buf, N, ch * K, K, n0);
         __builtin_amdgcn_sched_barrier(0);
     };
+    static_assert(KC % K == 0 && (!PIPE || KC == K), "checkpoint interval");
     // ckpt: true_type = this chunk is never the last (checkpoint unconditionally)
     auto step = [&](const raw (&buf)[K], int64_t ch, auto ckpt) {
         forward_rows<IO, SPK, RESET, V, K, VOUT, true, ALL>(c, in, buf, N, ch * K, K, n0, active, spikes, row_bytes,
                                                             v_out, v, y);
-        if ((decltype(ckpt)::value || ch < last) && (ALL || active)) store_f32<V>(saved + ch * N + n0, v);
+        if constexpr (KC == K) {
+            if ((decltype(ckpt)::value || ch < last) && (ALL || active)) store_f32<V>(saved + ch * N + n0, v);
+        } else {
+            const int64_t t_end = (ch + 1) * K;
+            if (t_end % KC == 0 && t_end < T && (ALL || active)) store_f32<V>(saved + (t_end / KC - 1) * N + n0, v);
+        }
     };
     constexpr std::true_type not_last{};
     constexpr std::false_type maybe_last{};
@@ -510,7 +517,7 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
 
 // Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
 // N load nothing and report no spikes; they exist only to complete spike-bit words.
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE>
 __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
                                                              const void* __restrict__ x,
                                                              uint8_t* __restrict__ spikes,
@@ -523,16 +530,16 @@ __global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, 
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
     const DenseIn<IO, V> in{x};
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                               v_in, v_last);
     else
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                                v_in, v_last);
 }
 
 // The same forward with the input current read from the previous layer's spikes through
 // the per-feature gain (neuron n has feature n % F).  Spikes in and out share the format.
-template <int IO, int SPK, int RESET, int V, int K, bool VOUT, bool PIPE>
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE>
 __global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_t T, int64_t N, int64_t F,
                                                                   const uint8_t* __restrict__ spikes_in,
                                                                   const float* __restrict__ gain,
@@ -547,10 +554,10 @@ __global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_
     in.row_bytes = row_bytes;
     in.init(gain, F, n0, n0 < N);
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                               nullptr, nullptr);
     else
-        forward_lanes<IO, SPK, RESET, V, K, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                                nullptr, nullptr);
 }
 

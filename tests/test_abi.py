@@ -64,8 +64,9 @@ def test_size_formulas(nat):
             for T in (33, 100, 256):
                 chunks = nat.snn_lif_saved_bytes(c, T, N) // (4 * N) + 1
                 assert -(-T // 32) <= chunks <= -(-T // 8)
-        # large layers use 16-step chunks
-        assert nat.snn_lif_saved_bytes(c, 256, 1 << 24) == 15 * (1 << 24) * 4
+        # large layers use 16-step chunks (fp32) or 32-step chunks (bf16)
+        K = 16 if io == "f32" else 32
+        assert nat.snn_lif_saved_bytes(c, 256, 1 << 24) == (256 // K - 1) * (1 << 24) * 4
         assert nat.snn_lif_saved_bytes(c, 0, 4096) == 0
         assert nat.snn_lif_saved_bytes(c, 100, 0) == 0
 

@@ -230,14 +230,15 @@ def test_gain_glue(H, io, spk, T, B, F):
 
 
 # Shapes that reach every lane/chunk plan of the library, run in full on the GPU and checked
-# on sampled neuron columns.  Backward lanes: fp32 2 neurons (1 when N is odd); bf16 4 on
-# layers of at least 2^20 neurons, else 2 or 1; the bf16 forward takes 8 per lane from 2^21.
-# Chunks: 16 steps (32 at 1 per lane), double-buffered below 2^20 lanes, a short tail chunk
-# when K does not divide T, and 4/8/16-step single chunks for short layers.
+# on sampled neuron columns.  Backward lanes: 2 neurons (1 when N is odd), bf16 4 on short
+# layers (T <= 16) of at least 2^20 neurons; the bf16 forward takes 8 per lane from 2^21.
+# Chunks: 16 steps (32 at 1 per lane, and for bf16 layers not double-buffered, whose forward
+# loads them 16 rows at a time), double-buffered below 2^20 lanes, a short tail chunk when
+# K does not divide T, and 4/8/16-step single chunks for short layers.
 PLAN_SHAPES = [
     (16, 1 << 20),          # one chunk (fp32 2 per lane, bf16 4)
-    (40, (1 << 20) + 4),    # fp32 double-buffered, tail; bf16 4 per lane, 3 chunks, tail
-    (40, 1 << 22),          # multi-chunk with a tail, not double-buffered (bf16 forward 8 per lane)
+    (40, (1 << 20) + 4),    # 2 per lane, double-buffered 16-step chunks, tail
+    (40, 1 << 22),          # not double-buffered: fp32 16-step, bf16 32-step chunks (forward 8 per lane)
     (16, 524290),           # 2 per lane, one chunk
     (40, 600002),           # 2 per lane, double-buffered, tail
     (40, 262145),           # 1 per lane (odd N), double-buffered 32-step chunks, tail
