@@ -248,6 +248,7 @@ PLAN_SHAPES = [
     (8, 524290),            # one 8-step chunk, 2 per lane
     (6, 1 << 22),           # 8-step chunk with a tail (bf16 forward: 8 per lane)
     (12, 262145),           # one 16-step chunk at 1 per lane (whose long chunk is 32 steps)
+    (24, 1 << 21),          # bf16: one 32-step chunk loaded as 16 rows + a tail; fp32: 16 + tail
 ]
 
 
