@@ -89,12 +89,27 @@ def backward(cfg: LifConfig, x: torch.Tensor, saved: torch.Tensor, grad_s: torch
     return grad_x
 
 
+def _check_gain_inputs(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, T: int, B: int, F: int):
+    N = B * F
+    if cfg.spk == "io":
+        _require(spikes_in.dtype == cfg.dtype and tuple(spikes_in.shape) == (T, N),
+                 f"spikes_in must be a {cfg.dtype} tensor of shape ({T}, {N})")
+    else:
+        row = native.snn_spike_row_bytes(cfg.c(), N)
+        _require(spikes_in.dtype == torch.uint8 and tuple(spikes_in.shape) == (T, row),
+                 f"spikes_in must be a uint8 tensor of shape ({T}, {row})")
+    _require(spikes_in.is_contiguous(), "spikes_in must be contiguous")
+    _require(gain.dtype == torch.float32 and gain.numel() == F and gain.is_contiguous(),
+             f"gain must be a contiguous float32 tensor of {F} values")
+
+
 def forward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, B: int, F: int, *,
                  v_out: bool = False, out=None, stream=None):
     """Forward of the layer fed gain[f] * spikes_in (the previous layer's spikes, this cfg's
     u8/bits format, [T][row_bytes]).  Returns (spikes, saved, v_or_None)."""
     T = spikes_in.shape[0]
     N = B * F
+    _check_gain_inputs(cfg, spikes_in, gain, T, B, F)
     spikes, saved, v = out if out is not None else alloc_forward(cfg, T, N, spikes_in.device, v_out)
     native.snn_lif_forward_gain(cfg.c(), T, B, F, spikes_in, gain, spikes, saved if saved.numel() else None, v,
                                 stream)
@@ -107,6 +122,7 @@ def backward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, s
     """Backward of forward_gain; returns dL/d spikes_in = gain[f] * dL/dx, [T][N] in cfg's I/O
     dtype (in place if grad_s_in is grad_s)."""
     T = spikes_in.shape[0]
+    _check_gain_inputs(cfg, spikes_in, gain, T, B, F)
     _require(grad_s.dtype == cfg.dtype and tuple(grad_s.shape) == (T, B * F) and grad_s.is_contiguous(),
              f"grad_s must be a contiguous {cfg.dtype} tensor of shape ({T}, {B * F})")
     if grad_s_in is None:
