@@ -119,3 +119,39 @@ def test_fused_stack_autograd(H, dtype):
     H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), gx, gm, rtol, rep)
     H.say(f"fused stack autograd {dtype}: {rep}")
     assert rep.ok(), str(rep)
+
+
+def test_training_reduces_loss(H):
+    """A small spiking network (Linear -> LIFLayer -> GainLIF -> mean over time -> Linear)
+    trained with Adam on a seeded synthetic two-class problem: the loss must fall, i.e. the
+    surrogate gradients through the fused kernels (and through the gain-fed layer into the
+    first layer) are usable for training."""
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import GainLIF, LIFLayer
+    g = torch.Generator(device="cpu").manual_seed(0)
+    T, B, D, Hd = 8, 256, 32, 128
+    centers = torch.randn(2, D, generator=g)
+    labels = torch.randint(0, 2, (B,), generator=g)
+    x = (centers[labels] + 0.8 * torch.randn(B, D, generator=g)).to(H.DEV)
+    labels = labels.to(H.DEV)
+    gain = 0.5 + 1.5 * torch.rand(Hd, generator=g)
+    torch.manual_seed(0)
+    model = torch.nn.ModuleDict({"fc1": torch.nn.Linear(D, Hd), "lif1": LIFLayer(0.5, 1.0),
+                                 "lif2": GainLIF(gain, 0.5, 1.0), "fc2": torch.nn.Linear(Hd, 2)}).to(H.DEV)
+    opt = torch.optim.Adam(model.parameters(), lr=3e-3)
+
+    def loss_fn():
+        cur = model["fc1"](x).unsqueeze(0).expand(T, B, Hd).contiguous()   # constant input current
+        s2 = model["lif2"](model["lif1"](cur))                             # spikes -> gain-fed layer
+        return torch.nn.functional.cross_entropy(model["fc2"](s2.mean(0)), labels)
+
+    first = loss_fn().item()
+    for _ in range(40):
+        opt.zero_grad()
+        loss = loss_fn()
+        loss.backward()
+        opt.step()
+    last = loss_fn().item()
+    H.say(f"training: loss {first:.4f} -> {last:.4f}")
+    assert model["fc1"].weight.grad is not None and torch.isfinite(model["fc1"].weight.grad).all()
+    assert np.isfinite(last) and last < 0.8 * first
