@@ -42,11 +42,15 @@ def bytes_per_nts(w):
     LIF forward: read x, write spikes; LIF backward: read x (recompute) and dL/dy, write
     dL/dx; gain forward: read spikes, write x_next; gain backward: read and write.  The
     gain-fed layer: forward reads the previous spikes and writes its own; backward reads
-    the previous spikes and dL/dy, writes dL/d(previous spikes)."""
+    the previous spikes and dL/dy, writes dL/d(previous spikes).  The stack fused across
+    depth counts per position of the stack, not per layer."""
     e = 4 if w.io == "f32" else 2
     s = 1.0 if w.spk == "u8" else 0.125
     return {"lif_forward": e + s, "lif_backward": 3 * e, "gain_forward": s + e, "gain_backward": 2 * e,
-            "lif_forward_gain": 2 * s, "lif_backward_gain": s + 2 * e}
+            "lif_forward_gain": 2 * s, "lif_backward_gain": s + 2 * e,
+            # the whole stack in one kernel, per position (t, n): x in and the last layer's
+            # spikes out; x and the last layer's dL/dy in, the first layer's dL/dx out
+            "lif_stack_forward": e + s, "lif_stack_backward": 3 * e}
 
 
 def source_hash() -> str:
@@ -264,6 +268,8 @@ def main():
     ap.add_argument("--T", type=int, default=None, help="override T (large workload sweep)")
     ap.add_argument("--fused-stack", action="store_true",
                     help="stack: layers after the first read the previous spikes through the gain")
+    ap.add_argument("--depth-stack", action="store_true",
+                    help="stack: every layer in one kernel per direction (fused across depth)")
     ap.add_argument("--graph-trials", type=int, default=None,
                     help="also time this many independent forward+backward trials replayed from one HIP "
                          "graph (default 1000 for the single workload, else off)")
@@ -344,6 +350,18 @@ def main():
     nts = T * N
 
     fused = args.fused_stack and L > 1
+    depth = args.depth_stack and L > 1
+    if depth:
+        gstack = torch.stack(gains).contiguous()
+        dsaved = native.snn_lif_stack_saved_bytes(c, L, T, N)
+        for st in sets:
+            st["dsaved"] = torch.empty(dsaved, dtype=torch.uint8, device=dev) if dsaved else None
+
+    def launches_depth(st):
+        return [("lif_stack_forward", bpn["lif_stack_forward"] * nts, lambda: native.snn_lif_stack_forward(
+                    c, L, T, B, F, st["x"][0], gstack, st["spk"][L - 1], None, st["dsaved"], None, s_ptr)),
+                ("lif_stack_backward", bpn["lif_stack_backward"] * nts, lambda: native.snn_lif_stack_backward(
+                    c, L, T, B, F, st["x"][0], gstack, st["dsaved"], st["gs"], st["g"][0], s_ptr))]
 
     def launches_fused(st):
         out = [("lif_forward", bpn["lif_forward"] * nts, lambda: native.snn_lif_forward(
@@ -363,6 +381,8 @@ def main():
 
     def launches(st):
         """The kernels of one step, in order: (kernel, algorithmic bytes, call)."""
+        if depth:
+            return launches_depth(st)
         if fused:
             return launches_fused(st)
         out = []
@@ -425,7 +445,7 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
 
-    wtag = f"{w.name}{'fused' if fused else ''}_T{T}_N{N}"
+    wtag = f"{w.name}{'depth' if depth else 'fused' if fused else ''}_T{T}_N{N}"
     # the dominant kernel: the largest share of the step's kernel time
     dom_name = max(kernels, key=lambda k: kernels[k]["avg_launch_ms"] * kernels[k]["launches_per_step"])
     dom = kernels[dom_name]
@@ -447,7 +467,8 @@ def main():
         "config": {"workload": w.description, "T": T, "N": N, "layers": L, "dims": list(w.dims), "io": w.io,
                    "spikes": w.spk, "reset": w.params.reset, "decay": w.params.decay,
                    "v_th": w.params.v_th, "alpha": w.params.alpha, "buffer_sets": R,
-                   "schedule": "fused across the gain" if fused else "layer by layer",
+                   "schedule": ("fused across depth" if depth else "fused across the gain" if fused
+                                else "layer by layer"),
                    "parallelism": "none (1 GPU)"},
         "hbm_fraction_step": step_bytes / (step_kernel_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"kernel": dom_name, "bound": "hbm", "achieved": dom["GB/s"],

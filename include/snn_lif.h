@@ -171,6 +171,35 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg *cfg, int64_t T, int64_t B, i
                                  const void *spikes_in, const float *gain, const void *saved,
                                  const void *grad_s, void *grad_s_in, void *stream);
 
+/* A stack of L = 2 or 3 LIF layers joined by per-feature gains, fused across the layers as
+ * well as across time: layer 0 is fed x, layer l > 0 is fed gain[l-1][f] * y_{l-1} of the
+ * same step, and one kernel per direction carries every neuron through all L layers with
+ * the L membranes on chip.  The layers are those of snn_gain_spikes_forward +
+ * snn_lif_forward applied in turn (same cfg for every layer); fusing across layers goes
+ * beyond the paper (Sec. 5 puts an ANN operator between layers) and is offered for this
+ * elementwise operator only.  Shapes as the gain functions: N = B*F, neuron (b, f) at b*F + f.
+ *   x          [T][N] io dtype: layer 0's input current.
+ *   gains      device float32 [L-1][F].  As in snn_lif_forward_gain, a gain multiplies a
+ *              spike after rounding to cfg->io, so spikes and membranes equal those of the
+ *              layer-by-layer run bit for bit.
+ *   spikes     [T][row_bytes] out: the last layer's spikes in cfg->spk format.
+ *   hidden_spikes  NULLABLE [L-1][T][row_bytes] out: the other layers' spikes.
+ *   saved      snn_lif_stack_saved_bytes() bytes out (every layer's membrane checkpoints;
+ *              may be NULL when that size is 0).
+ *   v_out      NULLABLE [L][T][N] float32 out: every layer's membranes (tests).
+ * backward: x, gains, saved exactly as in the forward; grad_s [T][N] io: dL/dy of the last
+ * layer; grad_x [T][N] io out: dL/dx of layer 0 (may be the same buffer as grad_s).  The
+ * gradient handed from layer l down to layer l-1, gain dL/dx_l, stays in fp32 (the
+ * layer-by-layer run stores it in the io dtype).  Other L: SNN_E_UNSUPPORTED. */
+snn_status snn_lif_stack_saved_bytes(const snn_lif_cfg *cfg, int32_t L, int64_t T, int64_t N,
+                                     size_t *bytes);
+snn_status snn_lif_stack_forward(const snn_lif_cfg *cfg, int32_t L, int64_t T, int64_t B, int64_t F,
+                                 const void *x, const float *gains, void *spikes,
+                                 void *hidden_spikes, void *saved, float *v_out, void *stream);
+snn_status snn_lif_stack_backward(const snn_lif_cfg *cfg, int32_t L, int64_t T, int64_t B,
+                                  int64_t F, const void *x, const float *gains, const void *saved,
+                                  const void *grad_s, void *grad_x, void *stream);
+
 /* Serial (per-time-step) baseline of the same layer: the "serial training" method that
  * temporal fusion is compared against (Sec. 3.2, Fig. 3) -- one launch per time step, the
  * membrane round-tripping through memory between steps.  Kept as an ablation baseline.

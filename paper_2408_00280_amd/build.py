@@ -1,8 +1,8 @@
 """Compile the HIP library libsnnlif.so for gfx950 (in-tree, next to this file).
 
 The kernel variants are split over several translation units (one per forward I/O dtype and
-spike format, one per backward I/O dtype, the same for the gain-fed layer, the gain
-kernels, the serial baseline, the C ABI) that compile in
+spike format, one per backward I/O dtype, the same for the gain-fed layer and for the
+stack fused across depth, the gain kernels, the serial baseline, the C ABI) that compile in
 parallel and link into one shared library.
 """
 from __future__ import annotations
@@ -34,6 +34,9 @@ UNITS = (
     + [(f"bwd_io{io}", "lif_backward.hip", [f"-DSNNLIF_IO={io}"]) for io in (0, 1)]
     + [(f"bwdgain_io{io}_spk{spk}", "lif_backward.hip", [f"-DSNNLIF_IO={io}", f"-DSNNLIF_SPK={spk}", "-DSNNLIF_GAIN=1"])
        for io in (0, 1) for spk in (0, 1, 2)]
+    + [(f"stackf_io{io}_spk{spk}", "lif_stack.hip", [f"-DSNNLIF_IO={io}", f"-DSNNLIF_SPK={spk}"])
+       for io in (0, 1) for spk in (0, 1, 2)]
+    + [(f"stackb_io{io}", "lif_stack.hip", [f"-DSNNLIF_IO={io}", "-DSNNLIF_STACK_BWD=1"]) for io in (0, 1)]
     + [("glue", "lif_glue.hip", []), ("serial", "lif_serial.hip", []), ("api", "snn_lif_api.hip", [])]
 )
 

@@ -92,6 +92,39 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     return p;
 }
 
+// A stack of L layers fused across depth (lif_stack_*_kernel): 2 neurons per lane (1 when
+// N is odd), 16-step chunks -- L membranes per neuron and step in the backward's VGPRs --
+// or the shortest of kShortChunks that holds a short layer.
+constexpr int kMaxStackLayers = 3;
+
+struct StackPlan {
+    int v;
+    int k;
+    int64_t lanes;
+    int64_t row_bytes;
+};
+
+inline StackPlan make_stack_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
+    StackPlan p;
+    p.v = N % 2 != 0 ? 1 : 2;
+    p.k = 16;
+    for (int k : kShortChunks) {
+        if (T <= k && k < p.k) {
+            p.k = k;
+            break;
+        }
+    }
+    p.row_bytes = spike_row_bytes(c, N);
+    const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
+    p.lanes = (covered + p.v - 1) / p.v;
+    return p;
+}
+
+inline int64_t stack_saved_bytes(const StackPlan& p, int L, int64_t T, int64_t N) {
+    const int64_t chunks = (T + p.k - 1) / p.k;
+    return chunks > 1 ? (chunks - 1) * L * N * int64_t(sizeof(float)) : 0;
+}
+
 inline int64_t saved_bytes(const Plan& p, int64_t T, int64_t N) {
     const int64_t chunks = (T + p.k - 1) / p.k;
     return chunks > 1 ? (chunks - 1) * N * int64_t(sizeof(float)) : 0;
@@ -202,6 +235,17 @@ template <int IO, int SPK>
 snn_status backward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
                                const void* spikes_in, const float* gain, const void* saved, const void* gs,
                                void* gs_in, hipStream_t s);
+
+// The stack fused across depth: gains is [L-1][F]; hidden and v_out may be null.
+template <int IO, int SPK>
+snn_status stack_forward_entry(int reset, int L, const StackPlan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
+                               const void* x, const float* gains, void* spikes, void* hidden, void* saved,
+                               float* v_out, hipStream_t s);
+
+template <int IO>
+snn_status stack_backward_entry(int reset, int L, const StackPlan& p, const LifK& k, int64_t T, int64_t N, int64_t F,
+                                const void* x, const float* gains, const void* saved, const void* gs, void* gx,
+                                hipStream_t s);
 
 snn_status gain_forward_entry(const snn_lif_cfg* c, int64_t T, int64_t N, int64_t F, const void* spikes,
                               int64_t row_bytes, const float* gain, void* x_next, hipStream_t s);

@@ -755,6 +755,246 @@ __global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64
 }
 
 // ------------------------------------------------------------------------------------
+// A stack of L layers fused across depth as well as time.  Layer 0 is fed x; layer l > 0 is
+// fed gain_{l-1}[f] y_{l-1} of the same step (neuron n has feature n % F), so one lane can
+// carry its neurons through every layer with all L membranes in VGPRs.  Only x, the last
+// layer's spikes, the checkpoints (all L membranes every K steps, saved[chunk][l][N]) and,
+// backward, the last layer's dL/dy and layer 0's dL/dx go through memory.  The gain is
+// rounded to the I/O dtype before it multiplies a spike, as a stored input current would
+// be; the gradient handed down a layer, gain dL/dx, stays in fp32.
+template <int V, int L>
+struct StackGains {
+    float gx[L - 1][V];   // rounded to the I/O dtype (forward input)
+    float gy[L - 1][V];   // fp32 (gradient handed down)
+    template <int IO>
+    __device__ void init(const float* gains, int64_t F, int64_t n0, bool active) {
+#pragma unroll
+        for (int l = 0; l < L - 1; ++l) {
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                gy[l][j] = active ? gains[l * F + (n0 + j) % F] : 0.0f;
+                gx[l][j] = IO == SNN_IO_BF16 ? bf16_lo(pack_bf16x2(gy[l][j], 0.0f)) : gy[l][j];
+            }
+        }
+    }
+};
+
+// One step of every layer; x0 is layer 0's input current.
+template <int RESET, int V, int L>
+__device__ __forceinline__ void stack_step(const LifK& c, const StackGains<V, L>& G, const float (&x0)[V],
+                                           float (&v)[L][V], bool (&y)[L][V]) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[0][j], y[0][j], x0[j]);
+#pragma unroll
+    for (int l = 1; l < L; ++l) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) lif_step<RESET>(c, v[l][j], y[l][j], G.gx[l - 1][j] * float(y[l - 1][j]));
+    }
+}
+
+// Forward of one workgroup's lanes, chunks of K steps (a short tail chunk last).  OUT: also
+// write the hidden layers' spikes (hidden[l][T][row_bytes]) and every layer's membrane
+// (v_out[l][T][N]) where those pointers are not null.
+template <int IO, int SPK, int RESET, int V, int K, int L, bool OUT, bool ALL>
+__device__ __forceinline__ void stack_forward_lanes(const LifK& c, const DenseIn<IO, V>& in,
+                                                    const StackGains<V, L>& G, int64_t T, int64_t N, int64_t n0,
+                                                    uint8_t* __restrict__ spikes, uint8_t* __restrict__ hidden,
+                                                    int64_t row_bytes, float* __restrict__ saved,
+                                                    float* __restrict__ v_out) {
+    using raw = typename DenseIn<IO, V>::raw;
+    const bool active = ALL || n0 < N;
+    float v[L][V];
+    bool y[L][V];
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            v[l][j] = c.rest;
+            y[l][j] = false;
+        }
+    }
+    const int64_t n_full = T / K;
+    const int k_tail = int(T % K);
+    const int64_t last = k_tail ? n_full : n_full - 1;
+    raw a[K];
+    auto rows = [&](int64_t t0, int kn, auto full) {
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+            if (decltype(full)::value || i < kn) {
+                float x0[V];
+#pragma unroll
+                for (int j = 0; j < V; ++j) x0[j] = active ? in.get(a[i], j, n0) : 0.0f;
+                stack_step<RESET, V, L>(c, G, x0, v, y);
+                const int64_t t = t0 + i;
+                SpikeOut<IO, SPK, V>::store(spikes, row_bytes, t, n0, active, y[L - 1]);
+                if constexpr (OUT) {
+                    if (hidden != nullptr) {
+#pragma unroll
+                        for (int l = 0; l < L - 1; ++l)
+                            SpikeOut<IO, SPK, V>::store(hidden + l * T * row_bytes, row_bytes, t, n0, active, y[l]);
+                    }
+                    if (v_out != nullptr && active) {
+#pragma unroll
+                        for (int l = 0; l < L; ++l) store_f32<V>(v_out + (l * T + t) * N + n0, v[l]);
+                    }
+                }
+            }
+        }
+    };
+    for (int64_t ch = 0; ch < n_full; ++ch) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (active) load_rows<DenseIn<IO, V>, K, true, false>(in, a, N, ch * K, K, n0);
+        __builtin_amdgcn_sched_barrier(0);
+        rows(ch * K, K, std::true_type{});
+        if (ch < last && active) {
+#pragma unroll
+            for (int l = 0; l < L; ++l) store_f32<V>(saved + (ch * L + l) * N + n0, v[l]);
+        }
+    }
+    if (k_tail) {
+        if (active) load_rows<DenseIn<IO, V>, K, false, false>(in, a, N, n_full * K, k_tail, n0);
+        rows(n_full * K, k_tail, std::false_type{});
+    }
+}
+
+// Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes (as the layer's
+// forward); gains is [L-1][F].
+template <int IO, int SPK, int RESET, int V, int K, int L, bool OUT>
+__global__ __launch_bounds__(kBlock) void lif_stack_forward_kernel(LifK c, int64_t T, int64_t N, int64_t F,
+                                                                   const void* __restrict__ x,
+                                                                   const float* __restrict__ gains,
+                                                                   uint8_t* __restrict__ spikes,
+                                                                   uint8_t* __restrict__ hidden,
+                                                                   int64_t row_bytes,
+                                                                   float* __restrict__ saved,
+                                                                   float* __restrict__ v_out) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    const DenseIn<IO, V> in{x};
+    StackGains<V, L> G;
+    G.template init<IO>(gains, F, n0, n0 < N);
+    if (first + kBlock * V <= N)
+        stack_forward_lanes<IO, SPK, RESET, V, K, L, OUT, true>(c, in, G, T, N, n0, spikes, hidden, row_bytes, saved,
+                                                                v_out);
+    else
+        stack_forward_lanes<IO, SPK, RESET, V, K, L, OUT, false>(c, in, G, T, N, n0, spikes, hidden, row_bytes,
+                                                                 saved, v_out);
+}
+
+// Backward of one chunk: recompute every layer's membranes from the state entering the
+// chunk (checkpoint or V_rest), then Eq. (3) in reverse time, the layers top-down within
+// each step: the gradient layer l hands down, gain_{l-1} g_l, is layer l-1's dL/dy of the
+// same step.  g[l] enters as dL/dv of layer l at the step after the chunk.
+template <int IO, int RESET, int V, int K, int L, bool FULL>
+__device__ __forceinline__ void stack_backward_chunk(const LifK& c, const DenseIn<IO, V>& in,
+                                                     const StackGains<V, L>& G,
+                                                     const typename IoVec<IO, V>::raw (&xr)[K],
+                                                     const typename IoVec<IO, V>::raw (&gr)[K],
+                                                     const float (&vc)[L][V], bool carried, int64_t N, int64_t t0,
+                                                     int kn, int64_t n0, void* gx, float (&g)[L][V]) {
+    using Io = IoVec<IO, V>;
+    float v[L][V];
+    bool y[L][V];
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+            v[l][j] = carried ? vc[l][j] : c.rest;
+            y[l][j] = carried && vc[l][j] >= c.th;
+        }
+    }
+    float vs[K][L][V];
+#pragma unroll
+    for (int i = 0; i < K; ++i) {
+        if (FULL || i < kn) {
+            float x0[V];
+#pragma unroll
+            for (int j = 0; j < V; ++j) x0[j] = in.get(xr[i], j, n0);
+            stack_step<RESET, V, L>(c, G, x0, v, y);
+#pragma unroll
+            for (int l = 0; l < L; ++l) {
+#pragma unroll
+                for (int j = 0; j < V; ++j) vs[i][l][j] = v[l][j];
+            }
+        }
+    }
+#pragma unroll
+    for (int i = K - 1; i >= 0; --i) {
+        if (FULL || i < kn) {
+            float out[V];
+#pragma unroll
+            for (int j = 0; j < V; ++j) {
+                float gs = Io::get(gr[i], j);
+#pragma unroll
+                for (int l = L - 1; l >= 0; --l) {
+                    const float vt = vs[i][l][j];
+                    const float d = surrogate(c, vt - c.th);
+                    float dv_next;
+                    if (RESET == SNN_RESET_HARD)  // k (1 - y^t) + (V_rest - k v^t) delta^t
+                        dv_next = fmaf(fmaf(-c.k, vt, c.rest), d, vt >= c.th ? 0.0f : c.k);
+                    else                          // k (1 - V_th delta^t)
+                        dv_next = fmaf(-c.kth, d, c.k);
+                    g[l][j] = fmaf(gs, d, dv_next * g[l][j]);
+                    if (l > 0) gs = G.gy[l - 1][j] * g[l][j];
+                }
+                out[j] = g[0][j];
+            }
+            Io::store(gx, (t0 + i) * N + n0, out);
+        }
+    }
+}
+
+template <int IO, int RESET, int V, int K, int L>
+__device__ __forceinline__ void stack_backward_lanes(const LifK& c, const DenseIn<IO, V>& in,
+                                                     const StackGains<V, L>& G, int64_t T, int64_t N, int64_t n0,
+                                                     const float* __restrict__ saved, const void* gs, void* gx) {
+    using raw = typename IoVec<IO, V>::raw;
+    float g[L][V];
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) g[l][j] = 0.0f;   // dL/dv^{T+1} = 0 in every layer
+    }
+    const int64_t n_full = T / K;
+    const int k_tail = int(T % K);
+    raw xr[K], gr[K];
+    float vc[L][V];
+    auto load = [&](int64_t ch, int kn, auto full) {
+        if (ch > 0) {
+#pragma unroll
+            for (int l = 0; l < L; ++l) load_f32<V>(saved + ((ch - 1) * L + l) * N + n0, vc[l]);
+        }
+        load_rows<DenseIn<IO, V>, K, decltype(full)::value, false>(in, xr, N, ch * K, kn, n0);
+        load_rows<DenseIn<IO, V>, K, decltype(full)::value, true>(DenseIn<IO, V>{gs}, gr, N, ch * K, kn, n0);
+    };
+    if (k_tail) {
+        load(n_full, k_tail, std::false_type{});
+        stack_backward_chunk<IO, RESET, V, K, L, false>(c, in, G, xr, gr, vc, n_full > 0, N, n_full * K, k_tail, n0,
+                                                        gx, g);
+    }
+    for (int64_t ch = n_full - 1; ch >= 0; --ch) {
+        __builtin_amdgcn_sched_barrier(0);
+        load(ch, K, std::true_type{});
+        __builtin_amdgcn_sched_barrier(0);
+        stack_backward_chunk<IO, RESET, V, K, L, true>(c, in, G, xr, gr, vc, ch > 0, N, ch * K, K, n0, gx, g);
+    }
+}
+
+template <int IO, int RESET, int V, int K, int L>
+__global__ __launch_bounds__(kBlock) void lif_stack_backward_kernel(LifK c, int64_t T, int64_t N, int64_t F,
+                                                                    const void* __restrict__ x,
+                                                                    const float* __restrict__ gains,
+                                                                    const float* __restrict__ saved,
+                                                                    const void* gs, void* gx) {
+    const int64_t first = xcd_contiguous_block() * kBlock * V;
+    const int64_t n0 = first + int64_t(threadIdx.x) * V;
+    if (first + kBlock * V > N && n0 >= N) return;
+    StackGains<V, L> G;
+    G.template init<IO>(gains, F, n0, true);
+    stack_backward_lanes<IO, RESET, V, K, L>(c, DenseIn<IO, V>{x}, G, T, N, n0, saved, gs, gx);
+}
+
+// ------------------------------------------------------------------------------------
 // Per-feature gain between stacked layers.  One lane per V neurons walks all T rows,
 // kGlueRows rows of loads in flight at a time.
 constexpr int kGlueRows = 8;

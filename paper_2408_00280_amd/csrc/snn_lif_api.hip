@@ -214,6 +214,75 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, i
     }
 }
 
+snn_status snn_lif_stack_saved_bytes(const snn_lif_cfg* cfg, int32_t L, int64_t T, int64_t N, size_t* bytes) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if (bytes == nullptr) return SNN_E_NULL;
+    if ((st = check_shape(T, N)) != SNN_OK) return st;
+    if (L < 2 || L > kMaxStackLayers) return SNN_E_UNSUPPORTED;
+    *bytes = (T == 0 || N == 0) ? 0 : size_t(stack_saved_bytes(make_stack_plan(cfg, T, N), L, T, N));
+    return SNN_OK;
+}
+
+snn_status snn_lif_stack_forward(const snn_lif_cfg* cfg, int32_t L, int64_t T, int64_t B, int64_t F, const void* x,
+                                 const float* gains, void* spikes, void* hidden_spikes, void* saved, float* v_out,
+                                 void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    if (L < 2 || L > kMaxStackLayers) return SNN_E_UNSUPPORTED;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    if (T > kMaxTN / (int64_t(L) * N)) return SNN_E_SHAPE;   // v_out holds L T N values
+    const StackPlan p = make_stack_plan(cfg, T, N);
+    const bool need_saved = stack_saved_bytes(p, L, T, N) > 0;
+    if (x == nullptr || gains == nullptr || spikes == nullptr || (need_saved && saved == nullptr)) return SNN_E_NULL;
+    if (!aligned(x) || !aligned(gains) || !aligned(spikes) || (hidden_spikes && !aligned(hidden_spikes)) ||
+        (saved && !aligned(saved)) || (v_out && !aligned(v_out)))
+        return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void* sv = need_saved ? saved : nullptr;
+    const int r = cfg->reset;
+    switch (cfg->io * 4 + cfg->spk) {
+        case SNN_IO_F32 * 4 + SNN_SPK_U8:
+            return stack_forward_entry<SNN_IO_F32, SNN_SPK_U8>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_BITS:
+            return stack_forward_entry<SNN_IO_F32, SNN_SPK_BITS>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+        case SNN_IO_F32 * 4 + SNN_SPK_IO:
+            return stack_forward_entry<SNN_IO_F32, SNN_SPK_IO>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_U8:
+            return stack_forward_entry<SNN_IO_BF16, SNN_SPK_U8>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+        case SNN_IO_BF16 * 4 + SNN_SPK_BITS:
+            return stack_forward_entry<SNN_IO_BF16, SNN_SPK_BITS>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+        default:
+            return stack_forward_entry<SNN_IO_BF16, SNN_SPK_IO>(r, L, p, k, T, N, F, x, gains, spikes, hidden_spikes, sv, v_out, s);
+    }
+}
+
+snn_status snn_lif_stack_backward(const snn_lif_cfg* cfg, int32_t L, int64_t T, int64_t B, int64_t F, const void* x,
+                                  const float* gains, const void* saved, const void* grad_s, void* grad_x,
+                                  void* stream) {
+    snn_status st = check_cfg(cfg);
+    if (st != SNN_OK) return st;
+    if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
+    if (L < 2 || L > kMaxStackLayers) return SNN_E_UNSUPPORTED;
+    const int64_t N = B * F;
+    if (T == 0 || N == 0) return SNN_OK;
+    const StackPlan p = make_stack_plan(cfg, T, N);
+    const bool need_saved = stack_saved_bytes(p, L, T, N) > 0;
+    if (x == nullptr || gains == nullptr || grad_s == nullptr || grad_x == nullptr || (need_saved && saved == nullptr))
+        return SNN_E_NULL;
+    if (!aligned(x) || !aligned(gains) || !aligned(grad_s) || !aligned(grad_x) || (saved && !aligned(saved)))
+        return SNN_E_ALIGN;
+    const LifK k = kernel_consts(cfg);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const void* sv = need_saved ? saved : nullptr;
+    return cfg->io == SNN_IO_F32
+               ? stack_backward_entry<SNN_IO_F32>(cfg->reset, L, p, k, T, N, F, x, gains, sv, grad_s, grad_x, s)
+               : stack_backward_entry<SNN_IO_BF16>(cfg->reset, L, p, k, T, N, F, x, gains, sv, grad_s, grad_x, s);
+}
+
 snn_status snn_lif_serial_forward_step(const snn_lif_cfg* cfg, int64_t N, const void* x_t, const float* v_prev,
                                        float* v_t, void* spikes_t, void* stream) {
     snn_status st = check_cfg(cfg);

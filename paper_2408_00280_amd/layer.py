@@ -130,3 +130,40 @@ def backward_gain(cfg: LifConfig, spikes_in: torch.Tensor, gain: torch.Tensor, s
     native.snn_lif_backward_gain(cfg.c(), T, B, F, spikes_in, gain, saved if saved.numel() else None, grad_s,
                                  grad_s_in, stream)
     return grad_s_in
+
+
+def stack_forward(cfg: LifConfig, x: torch.Tensor, gains: torch.Tensor, B: int, F: int, *, hidden: bool = False,
+                  v_out: bool = False, stream=None):
+    """Forward of len(gains) + 1 layers fused across depth (gains: float32 [L-1, F]) on
+    x[T, ...] (cfg.dtype, N = B*F per step).  Returns (spikes of the last layer, hidden
+    spikes [L-1, T, ...] or None, saved, membranes [L, T, N] or None)."""
+    _require(x.dtype == cfg.dtype and x.is_contiguous(), f"x must be a contiguous {cfg.dtype} tensor")
+    _require(gains.dtype == torch.float32 and gains.dim() == 2 and gains.shape[1] == F and gains.is_contiguous(),
+             f"gains must be a contiguous float32 tensor of shape (L-1, {F})")
+    T, N = _TN(x)
+    _require(N == B * F, "x must hold B*F neurons per step")
+    L = gains.shape[0] + 1
+    c = cfg.c()
+    row = native.snn_spike_row_bytes(c, N)
+    shape = (T, N) if cfg.spk == "io" else (T, row)
+    sdt = cfg.dtype if cfg.spk == "io" else torch.uint8
+    spikes = torch.empty(shape, dtype=sdt, device=x.device)
+    hid = torch.empty((L - 1, *shape), dtype=sdt, device=x.device) if hidden else None
+    saved = torch.empty(native.snn_lif_stack_saved_bytes(c, L, T, N), dtype=torch.uint8, device=x.device)
+    v = torch.empty((L, T, N), dtype=torch.float32, device=x.device) if v_out else None
+    native.snn_lif_stack_forward(c, L, T, B, F, x, gains, spikes, hid, saved if saved.numel() else None, v, stream)
+    return spikes, hid, saved, v
+
+
+def stack_backward(cfg: LifConfig, x: torch.Tensor, gains: torch.Tensor, saved: torch.Tensor, grad_s: torch.Tensor,
+                   B: int, F: int, *, grad_x: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Backward of stack_forward: dL/dx of layer 0 from dL/dy of the last layer."""
+    _require(grad_s.dtype == cfg.dtype and grad_s.shape == x.shape and grad_s.is_contiguous(),
+             f"grad_s must be a contiguous {cfg.dtype} tensor shaped like x")
+    T, N = _TN(x)
+    L = gains.shape[0] + 1
+    if grad_x is None:
+        grad_x = torch.empty_like(grad_s)
+    native.snn_lif_stack_backward(cfg.c(), L, T, B, F, x, gains, saved if saved.numel() else None, grad_s, grad_x,
+                                  stream)
+    return grad_x

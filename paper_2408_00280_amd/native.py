@@ -31,7 +31,8 @@ STATUS_NAMES = {0: "SNN_OK", -1: "SNN_E_NULL", -2: "SNN_E_SHAPE", -3: "SNN_E_PAR
 EXPORTS = ("snn_spike_row_bytes", "snn_lif_saved_bytes", "snn_lif_forward", "snn_lif_backward",
            "snn_lif_forward_seg", "snn_lif_backward_seg",
            "snn_gain_spikes_forward", "snn_gain_grad_backward", "snn_lif_forward_gain",
-           "snn_lif_backward_gain", "snn_lif_serial_forward_step",
+           "snn_lif_backward_gain", "snn_lif_stack_saved_bytes", "snn_lif_stack_forward",
+           "snn_lif_stack_backward", "snn_lif_serial_forward_step",
            "snn_lif_serial_backward_step", "snn_status_str")
 
 
@@ -74,6 +75,9 @@ def _load():
         "snn_gain_grad_backward": [C, i64, i64, i64, vp, vp, vp, vp],
         "snn_lif_forward_gain": [C, i64, i64, i64, vp, vp, vp, vp, vp, vp],
         "snn_lif_backward_gain": [C, i64, i64, i64, vp, vp, vp, vp, vp, vp],
+        "snn_lif_stack_saved_bytes": [C, ctypes.c_int32, i64, i64, szp],
+        "snn_lif_stack_forward": [C, ctypes.c_int32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp],
+        "snn_lif_stack_backward": [C, ctypes.c_int32, i64, i64, i64, vp, vp, vp, vp, vp, vp],
         "snn_lif_serial_forward_step": [C, i64, vp, vp, vp, vp, vp],
         "snn_lif_serial_backward_step": [C, i64, vp, vp, vp, vp, vp, vp],
     }
@@ -169,6 +173,24 @@ def snn_lif_forward_gain(cfg, T, B, F, spikes_in, gain, spikes, saved, v_out=Non
 def snn_lif_backward_gain(cfg, T, B, F, spikes_in, gain, saved, grad_s, grad_s_in, stream=None):
     _check("snn_lif_backward_gain", lib.snn_lif_backward_gain(
         ctypes.byref(cfg), T, B, F, _ptr(spikes_in), _ptr(gain), _ptr(saved), _ptr(grad_s), _ptr(grad_s_in),
+        _stream(stream)))
+
+
+def snn_lif_stack_saved_bytes(cfg: snn_lif_cfg, L: int, T: int, N: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check("snn_lif_stack_saved_bytes", lib.snn_lif_stack_saved_bytes(ctypes.byref(cfg), L, T, N, ctypes.byref(out)))
+    return out.value
+
+
+def snn_lif_stack_forward(cfg, L, T, B, F, x, gains, spikes, hidden_spikes, saved, v_out=None, stream=None):
+    _check("snn_lif_stack_forward", lib.snn_lif_stack_forward(
+        ctypes.byref(cfg), L, T, B, F, _ptr(x), _ptr(gains), _ptr(spikes), _ptr(hidden_spikes), _ptr(saved),
+        _ptr(v_out), _stream(stream)))
+
+
+def snn_lif_stack_backward(cfg, L, T, B, F, x, gains, saved, grad_s, grad_x, stream=None):
+    _check("snn_lif_stack_backward", lib.snn_lif_stack_backward(
+        ctypes.byref(cfg), L, T, B, F, _ptr(x), _ptr(gains), _ptr(saved), _ptr(grad_s), _ptr(grad_x),
         _stream(stream)))
 
 

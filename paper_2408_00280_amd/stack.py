@@ -2,13 +2,16 @@
 the ANN operator between spiking layers), run layer by layer in temporal-major order:
 each layer's fused kernel covers all T steps before the next layer starts (Sec. 3.2).
 
-Two schedules:
+Three schedules:
   * unfused -- gain kernels between the layers materialise every layer's input current
     x and, in the backward, every layer's dL/dx;
   * fused   -- layers after the first read the previous layer's spikes and the gain
     directly (snn_lif_forward_gain), and their backward emits dL/d(previous spikes)
-    (snn_lif_backward_gain); no x or dL/dx beyond the first layer's is stored.
-Both give the same spikes, membranes and checkpoints bit for bit.
+    (snn_lif_backward_gain); no x or dL/dx beyond the first layer's is stored;
+  * depth   -- one kernel per direction runs every layer (snn_lif_stack_forward /
+    backward, 2 or 3 layers): only x, the last layer's spikes, the checkpoints and dL/dx
+    of the first layer go through memory.
+All give the same spikes and membranes bit for bit.
 
 Torch allocates; every step runs in the HIP kernels behind the C ABI.
 """
@@ -47,6 +50,21 @@ def forward(cfg: layer.LifConfig, x1: torch.Tensor, gains: list[torch.Tensor], B
             native.snn_gain_spikes_forward(cfg.c(), T, B, F, spikes, gains[l], x_next, stream)
             x = x_next
     return states
+
+
+def forward_depth(cfg: layer.LifConfig, x1: torch.Tensor, gains: list[torch.Tensor], B: int, F: int, *,
+                  hidden: bool = False, v_out: bool = False, stream=None):
+    """The whole stack in one forward kernel.  Returns (spikes of the last layer, hidden
+    spikes or None, saved, membranes or None, the stacked gains to pass to the backward)."""
+    g = torch.stack([t.to(torch.float32) for t in gains]).contiguous()
+    spikes, hid, saved, v = layer.stack_forward(cfg, x1, g, B, F, hidden=hidden, v_out=v_out, stream=stream)
+    return spikes, hid, saved, v, g
+
+
+def backward_depth(cfg: layer.LifConfig, x1: torch.Tensor, g: torch.Tensor, saved: torch.Tensor,
+                   grad_s_last: torch.Tensor, B: int, F: int, *, stream=None) -> torch.Tensor:
+    """dL/dx of the first layer from dL/dy of the last, in one backward kernel."""
+    return layer.stack_backward(cfg, x1, g, saved, grad_s_last, B, F, stream=stream)
 
 
 def backward(cfg: layer.LifConfig, states: list[LayerState], grad_s_last: torch.Tensor,

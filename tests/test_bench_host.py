@@ -22,10 +22,12 @@ def test_bytes_per_nts():
     bf = bench.bytes_per_nts(W.WORKLOADS["large"])
     assert bf["lif_forward"] == 2.125 and bf["lif_backward"] == 6
     assert bf["lif_forward_gain"] == 0.25 and bf["lif_backward_gain"] == 4.125
-    # a 3-layer stack moves 77 B per position layer by layer, 39 B fused across the gain
+    # a 3-layer stack moves 77 B per position layer by layer, 39 B fused across the gain,
+    # 17 B fused across depth
     unfused = 3 * (f32["lif_forward"] + f32["lif_backward"]) + 2 * (f32["gain_forward"] + f32["gain_backward"])
     fused = f32["lif_forward"] + f32["lif_backward"] + 2 * (f32["lif_forward_gain"] + f32["lif_backward_gain"])
-    assert (unfused, fused) == (77, 39)
+    depth = f32["lif_stack_forward"] + f32["lif_stack_backward"]
+    assert (unfused, fused, depth) == (77, 39, 17)
 
 
 def test_more_than_one_gpu_is_refused():

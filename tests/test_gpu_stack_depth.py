@@ -1,0 +1,153 @@
+"""GPU parity of the stack fused across depth (snn_lif_stack_forward / backward): 2 or 3
+layers joined by per-feature gains in one kernel per direction.  Every layer's spikes and
+membranes against the oracle run layer by layer (spikes exact, membranes bit for bit; the
+gain rounded to the I/O dtype as a stored input current would be), dL/dx of the first
+layer within rtol * bound; and, for fp32 I/O, every output bit for bit equal to the
+schedule that fuses each layer with its gain (snn_lif_forward_gain / backward_gain)."""
+import itertools
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def H():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from tests import gpu_harness
+    return gpu_harness
+
+
+def _round_io(H, a, io):
+    return H.parity.bf16_to_f32(H.synth_bf16(a)) if io == "bf16" else a
+
+
+def _oracle(H, p, x_np, gs_np, gains, B, F, io):
+    """Layer-by-layer oracle: per layer (y, v); dL/dx of layer 0 and its bound."""
+    P = H.oracle.Params.of(p)
+    L = len(gains) + 1
+    xs, ys, vs = [x_np], [], []
+    for l in range(L):
+        y, v = H.oracle.forward(P, xs[l])
+        ys.append(y)
+        vs.append(v)
+        if l < L - 1:
+            xs.append(_round_io(H, H.oracle.gain_forward(y, gains[l], B, F), io))
+    gy, gym = gs_np.astype(np.float64), np.abs(gs_np.astype(np.float64))
+    for l in range(L - 1, -1, -1):
+        gx, gm = H.oracle.backward(P, vs[l], ys[l], gy, gym)
+        if l > 0:
+            gy, gym = H.oracle.gain_backward(gx, gm, gains[l - 1], B, F)
+    return ys, vs, gx, gm
+
+
+def _spikes(H, t, N, spk):
+    return H.parity.unpack_spikes(H.to_host_f32(t) if spk == "io" else t.cpu().numpy(), N, spk)
+
+
+def _run(H, T, B, F, L, reset, io, spk, seed, n_sample=None, inplace=False):
+    torch = H.torch
+    from paper_2408_00280_amd import stack
+    N = B * F
+    p = H.W.LifParams(0.5, 1.0, reset=reset)
+    w = H.W.custom(f"depth{T}x{N}", T, N, p, seed=seed, io=io, spk=spk, x_dist=("normal", 0.5, 0.6))
+    cfg = H.cfg_of(w)
+    rng = np.random.default_rng(seed)
+    gains = [rng.uniform(-0.3, 1.8, size=F).astype(np.float32) for _ in range(L - 1)]
+    if n_sample is None:
+        x_np, gs_np = H.W.x_full(w), H.W.gs_full(w)
+        x, gs = H.to_dev(x_np, io), H.to_dev(gs_np, io)
+    else:
+        x, gs = H.upload_rows(w, "x"), H.upload_rows(w, "gs")
+    gdev = [torch.from_numpy(g).to(H.DEV) for g in gains]
+    spikes, hid, saved, v, gstack = stack.forward_depth(cfg, x, gdev, B, F, hidden=True, v_out=True)
+    if inplace:
+        gx = H.layer.stack_backward(cfg, x, gstack, saved, gs, B, F, grad_x=gs)
+    else:
+        gx = stack.backward_depth(cfg, x, gstack, saved, gs, B, F)
+    torch.cuda.synchronize()
+
+    if io == "f32" and n_sample is None and not inplace:   # bit for bit against the gain-fused schedule
+        states = stack.forward(cfg, x, gdev, B, F, v_out=True, fused=True)
+        grads = stack.backward(cfg, states, H.to_dev(gs_np, io), gdev, B, F)
+        torch.cuda.synchronize()
+        assert torch.equal(spikes, states[-1].spikes)
+        for l in range(L - 1):
+            assert torch.equal(hid[l], states[l].spikes), f"layer {l} spikes"
+        for l in range(L):
+            assert torch.equal(v[l].view(torch.int32), states[l].v.view(torch.int32)), f"layer {l} membranes"
+        assert torch.equal(gx.view(torch.int32), grads[0].view(torch.int32)), "dL/dx of layer 0"
+
+    cols = None if n_sample is None else H.sample_columns(N, n_sample, seed=seed)
+    if cols is None:
+        ys, vs, g_ref, bound = _oracle(H, p, x_np, gs_np, gains, B, F, io)
+        take = (lambda a: a)
+    else:
+        xc, gc = H.W.x_cols(w, cols), H.W.gs_cols(w, cols)
+        ys, vs, g_ref, bound = _oracle(H, p, xc, gc, [g[cols % F] for g in gains], 1, cols.size, io)
+        take = (lambda a: a[:, cols])
+    rep = H.parity.Report()
+    for l in range(L):
+        y_gpu = _spikes(H, spikes if l == L - 1 else hid[l], N, spk)
+        H.parity.compare_forward(take(y_gpu), ys[l], vs[l], p.v_th, v_gpu=take(v[l].cpu().numpy()), rep=rep)
+    rtol = H.parity.RTOL_BF16 if io == "bf16" else H.parity.RTOL_F32
+    H.parity.compare_grad(take(H.to_host_f32(gx)), g_ref, bound, rtol, rep)
+    return rep
+
+
+COMBOS = list(itertools.product([2, 3], ["hard", "soft"], ["f32", "bf16"], ["u8", "bits", "io"]))
+SMALL = [(1, 1, 1), (3, 2, 5), (16, 4, 1000), (17, 3, 333), (40, 7, 1001), (64, 2, 4096)]
+
+
+@pytest.mark.parametrize("T,B,F", SMALL, ids=lambda v: str(v))
+@pytest.mark.parametrize("L,reset,io,spk", COMBOS, ids=lambda v: str(v))
+def test_depth_stack_small(H, T, B, F, L, reset, io, spk):
+    rep = _run(H, T, B, F, L, reset, io, spk, seed=T * 100 + B + F + L)
+    assert rep.ok(), str(rep)
+
+
+# the stack workload's shape, plus larger layers checked on sampled columns: 2 and 1
+# neurons per lane, several chunks with a tail, short single chunks
+PLANS = [(32, 128, 4096, None), (40, 256, 4096, 1 << 12), (40, 3, 349525, 1 << 12), (4, 512, 4096, 1 << 12),
+         (9, 1, (1 << 20) + 1, 1 << 12)]
+
+
+@pytest.mark.parametrize("T,B,F,n_sample", PLANS, ids=lambda v: str(v))
+@pytest.mark.parametrize("L,reset,io,spk", [(3, "hard", "f32", "u8"), (3, "soft", "bf16", "bits"),
+                                            (2, "hard", "bf16", "io"), (3, "hard", "f32", "bits")],
+                         ids=lambda v: str(v))
+def test_depth_stack_plans(H, T, B, F, n_sample, L, reset, io, spk):
+    rep = _run(H, T, B, F, L, reset, io, spk, seed=T + B + F, n_sample=n_sample)
+    H.say(f"depth stack T={T} N={B * F} L={L} {reset} {io} {spk}: {rep}")
+    assert rep.ok(), str(rep)
+    H.torch.cuda.empty_cache()
+
+
+def test_depth_stack_in_place(H):
+    for io in ("f32", "bf16"):
+        rep = _run(H, 37, 5, 800, 3, "hard", io, "u8", seed=9, inplace=True)
+        assert rep.ok(), str(rep)
+
+
+def test_depth_stack_errors(H):
+    torch = H.torch
+    nat = H.native
+    cfg = H.layer.LifConfig(0.5, 1.0)
+    T, B, F = 40, 2, 64
+    x = torch.zeros((T, B * F), device=H.DEV)
+    g = torch.ones((2, F), device=H.DEV)
+    sp = torch.empty((T, B * F), dtype=torch.uint8, device=H.DEV)
+    for L in (1, 4):
+        with pytest.raises(nat.SnnError) as e:
+            nat.snn_lif_stack_forward(cfg.c(), L, T, B, F, x, g, sp, None, None)
+        assert e.value.status == -5
+    with pytest.raises(nat.SnnError) as e:   # 40 steps need checkpoints
+        nat.snn_lif_stack_forward(cfg.c(), 3, T, B, F, x, g, sp, None, None)
+    assert e.value.status == -1
+    assert nat.snn_lif_stack_saved_bytes(cfg.c(), 3, T, B * F) == 2 * 3 * B * F * 4
+    assert nat.snn_lif_stack_saved_bytes(cfg.c(), 2, 16, B * F) == 0
+    nat.snn_lif_stack_forward(cfg.c(), 3, 0, B, F, None, None, None, None, None)
+    torch.cuda.synchronize()
