@@ -114,3 +114,56 @@ class GainLIF(torch.nn.Module):
     def extra_repr(self) -> str:
         return (f"features={self.gain.numel()}, decay={self.decay}, v_th={self.v_th}, v_reset={self.v_reset}, "
                 f"alpha={self.alpha}, reset={self.reset}")
+
+
+class FusedLIFStack(torch.autograd.Function):
+    """len(gains) + 1 LIF layers joined by fixed per-feature gains, fused across depth and
+    time: one kernel per direction for the whole stack.  Returns the last layer's spikes;
+    the backward returns dL/dx of the first layer (the gains get no gradient)."""
+
+    @staticmethod
+    def forward(ctx, x: torch.Tensor, gains: torch.Tensor, cfg: layer.LifConfig):
+        if x.dtype not in _IO or cfg.io != _IO[x.dtype] or cfg.spk != "io":
+            raise TypeError("FusedLIFStack takes float32/bfloat16 input and a cfg with io matching it and spk='io'")
+        F = gains.shape[1]
+        if x.shape[-1] != F:
+            raise ValueError("gains must have one column per feature (the last axis of x)")
+        xc = x.contiguous()
+        T = xc.shape[0]
+        B = xc.numel() // (T * F) if T else 0
+        x2 = xc.view(T, B * F)
+        g = gains.to(torch.float32).contiguous()
+        spikes, _, saved, _ = layer.stack_forward(cfg, x2, g, B, F)
+        ctx.save_for_backward(x2, g, saved)
+        ctx.cfg, ctx.shape, ctx.BF = cfg, x.shape, (B, F)
+        return spikes.view(x.shape)
+
+    @staticmethod
+    def backward(ctx, grad_y: torch.Tensor):
+        x2, g, saved = ctx.saved_tensors
+        B, F = ctx.BF
+        gy = grad_y.to(x2.dtype).contiguous().view(x2.shape)
+        grad_x = layer.stack_backward(ctx.cfg, x2, g, saved, gy, B, F)
+        return grad_x.view(ctx.shape), None, None
+
+
+class LIFStack(torch.nn.Module):
+    """2 or 3 LIF layers joined by fixed per-feature gains (gains: [L-1, F], the feature axis
+    last), run as one fused kernel per direction: the same spikes as LIFLayer followed by
+    GainLIF layers, without their intermediate tensors."""
+
+    def __init__(self, gains: torch.Tensor, decay: float, v_th: float, v_reset: float = 0.0, alpha: float = 4.0,
+                 reset: str = "hard"):
+        super().__init__()
+        self.register_buffer("gains", gains.detach().to(torch.float32).contiguous())
+        self.decay, self.v_th, self.v_reset, self.alpha, self.reset = decay, v_th, v_reset, alpha, reset
+
+    def cfg(self, dtype: torch.dtype) -> layer.LifConfig:
+        return layer.LifConfig(self.decay, self.v_th, self.v_reset, self.alpha, self.reset, _IO[dtype], "io")
+
+    def forward(self, x: torch.Tensor) -> torch.Tensor:
+        return FusedLIFStack.apply(x, self.gains, self.cfg(x.dtype))
+
+    def extra_repr(self) -> str:
+        return (f"layers={self.gains.shape[0] + 1}, features={self.gains.shape[1]}, decay={self.decay}, "
+                f"v_th={self.v_th}, v_reset={self.v_reset}, alpha={self.alpha}, reset={self.reset}")

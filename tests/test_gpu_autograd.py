@@ -155,3 +155,37 @@ def test_training_reduces_loss(H):
     H.say(f"training: loss {first:.4f} -> {last:.4f}")
     assert model["fc1"].weight.grad is not None and torch.isfinite(model["fc1"].weight.grad).all()
     assert np.isfinite(last) and last < 0.8 * first
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lif_stack_module(H, dtype):
+    """LIFStack (the stack fused across depth) against LIFLayer -> GainLIF -> GainLIF: the
+    same last-layer spikes bit for bit, and x.grad bit for bit in fp32 (within the bf16
+    tolerance of the chain's own error in bf16, whose handed-down gradients are rounded)."""
+    torch = H.torch
+    from paper_2408_00280_amd.autograd import GainLIF, LIFLayer, LIFStack
+    T, B, F = 20, 4, 777
+    p = H.W.LifParams(0.5, 1.0, reset="soft")
+    w = H.W.custom("lstack", T, B * F, p, seed=47, io=dtype, spk="io", x_dist=("normal", 0.5, 0.6))
+    rng = np.random.default_rng(8)
+    gains = torch.from_numpy(rng.uniform(0.5, 2.0, size=(2, F)).astype(np.float32))
+    gs = H.to_dev(H.W.gs_full(w), dtype).view(T, B, F)
+    outs = []
+    for fused in (True, False):
+        x = H.to_dev(H.W.x_full(w), dtype).view(T, B, F).requires_grad_(True)
+        if fused:
+            model = LIFStack(gains, p.decay, p.v_th, reset="soft").to(H.DEV)
+        else:
+            model = torch.nn.Sequential(LIFLayer(p.decay, p.v_th, reset="soft"),
+                                        GainLIF(gains[0], p.decay, p.v_th, reset="soft"),
+                                        GainLIF(gains[1], p.decay, p.v_th, reset="soft")).to(H.DEV)
+        y = model(x)
+        (y * gs).sum().backward()
+        outs.append((y.detach(), x.grad))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0], outs[1][0])
+    if dtype == "f32":
+        assert torch.equal(outs[0][1].view(torch.int32), outs[1][1].view(torch.int32))
+    else:
+        a, b = H.to_host_f32(outs[0][1]), H.to_host_f32(outs[1][1])
+        assert np.all(np.abs(a - b) <= 4e-2 * np.maximum(np.abs(a), np.abs(b)) + 1e-3)
