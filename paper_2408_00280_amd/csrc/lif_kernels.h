@@ -1091,6 +1091,133 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
     for (; t0 < T; ++t0) emit(Io::load(gx_next, t0 * N + n0), t0);
 }
 
+// ------------------------------------------------------------------------------------
+// The same gain over a flat layout.  When every row is whole (N a multiple of the piece
+// width W, spike rows without padding) the [T][N] tensors are one contiguous run of T*N
+// elements and the gain is elementwise: element e belongs to feature e % F, N being a
+// multiple of F.  Lanes then stream consecutive 16-byte pieces of the whole run, the
+// access pattern of a plain copy, instead of walking rows N elements apart.  F is a
+// multiple of W, so a piece never wraps around the features and its W gains are one
+// aligned vector load; a lane loads the gains of all its pieces before their data, so
+// that the in-order wait counter never holds a piece's arithmetic behind a later load.
+constexpr int kFlatPieces = 8;   // pieces per lane, all loads in flight together
+
+template <int IO>
+constexpr int flat_width() { return IO == SNN_IO_F32 ? 4 : 8; }   // elements per 16-byte output piece
+
+template <int W>
+struct FlatGains {
+    float g[W];
+    __device__ void load(const float* gain, int64_t f) {
+#pragma unroll
+        for (int h = 0; h < W / 4; ++h) {
+            const f32x4_t v = *reinterpret_cast<const f32x4_t*>(gain + f + 4 * h);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) g[4 * h + j] = v[j];
+        }
+    }
+};
+
+// The spikes of one piece (W consecutive elements from element e) as one raw word.
+template <int IO, int SPK>
+struct FlatSpikes {   // SNN_SPK_IO: 0/1 in the I/O dtype
+    using Io = IoVec<IO, flat_width<IO>()>;
+    using raw = typename Io::raw;
+    __device__ static raw load(const uint8_t* s, int64_t e) { return Io::load(s, e); }
+    __device__ static float get(const raw& r, int j) { return Io::get(r, j); }
+};
+
+template <int IO>
+struct FlatSpikes<IO, SNN_SPK_U8> {
+    static constexpr int W = flat_width<IO>();
+    using raw = std::conditional_t<W == 4, uint32_t, uint64_t>;
+    __device__ static raw load(const uint8_t* s, int64_t e) { return *reinterpret_cast<const raw*>(s + e); }
+    __device__ static float get(const raw& r, int j) { return float(uint32_t(r >> (8 * j)) & 0xffu); }
+};
+
+template <int IO>
+struct FlatSpikes<IO, SNN_SPK_BITS> {   // W bits of byte e / 8, from bit e % 8 (0, or 4 when W = 4)
+    using raw = uint32_t;
+    __device__ static raw load(const uint8_t* s, int64_t e) { return uint32_t(s[e >> 3]) >> (e & 7); }
+    __device__ static float get(const raw& r, int j) { return float((r >> j) & 1u); }
+};
+
+// Runs emit(raw, gains, e) over the lane's pieces, e the piece's first element.  A lane's
+// pieces are kBlock pieces apart, so a wave touches one contiguous kilobyte per piece and
+// a workgroup one contiguous run.  Workgroups take the runs in launch order, i.e. dealt
+// round-robin over the XCDs: for this flat stream that measured faster than giving each
+// XCD one contiguous range, as the row walks do (stack workload, gain backward 26.6 vs
+// 28.4 us).  `step` = kBlock * W % F, precomputed by the host.
+template <int W, typename Raw, typename Load, typename Emit>
+__device__ __forceinline__ void flat_pieces(int64_t pieces, int64_t F, int64_t step, const float* gain, Load load,
+                                            Emit emit) {
+    const int64_t base = int64_t(blockIdx.x) * (kBlock * kFlatPieces);
+    const int64_t p0 = base + threadIdx.x;
+    int64_t f = (p0 * W) % F;
+    FlatGains<W> g[kFlatPieces];
+    Raw r[kFlatPieces];
+    if (base + kBlock * kFlatPieces <= pieces) {   // the whole workgroup inside: no per-lane guards
+#pragma unroll
+        for (int u = 0; u < kFlatPieces; ++u) {
+            g[u].load(gain, f);
+            f += step;
+            if (f >= F) f -= F;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kFlatPieces; ++u) r[u] = load((p0 + u * kBlock) * W);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kFlatPieces; ++u) emit(r[u], g[u], (p0 + u * kBlock) * W);
+    } else {
+#pragma unroll
+        for (int u = 0; u < kFlatPieces; ++u) {
+            const int64_t p = p0 + u * kBlock;
+            if (p < pieces) {
+                g[u].load(gain, f);
+                emit(load(p * W), g[u], p * W);
+            }
+            f += step;
+            if (f >= F) f -= F;
+        }
+    }
+}
+
+template <int IO, int SPK>
+__global__ __launch_bounds__(kBlock) void gain_forward_flat_kernel(int64_t pieces, int64_t F, int64_t step,
+                                                                   const uint8_t* __restrict__ spikes,
+                                                                   const float* __restrict__ gain,
+                                                                   void* __restrict__ x_next) {
+    constexpr int W = flat_width<IO>();
+    using In = FlatSpikes<IO, SPK>;
+    flat_pieces<W, typename In::raw>(
+        pieces, F, step, gain, [&](int64_t e) { return In::load(spikes, e); },
+        [&](const typename In::raw& r, const FlatGains<W>& g, int64_t e) {
+            float out[W];
+#pragma unroll
+            for (int j = 0; j < W; ++j) out[j] = g.g[j] * In::get(r, j);
+            IoVec<IO, W>::store(x_next, e, out);
+        });
+}
+
+// gx_next and gs may be the same buffer: every element is read and written by one lane,
+// its load first.
+template <int IO>
+__global__ __launch_bounds__(kBlock) void gain_backward_flat_kernel(int64_t pieces, int64_t F, int64_t step,
+                                                                    const void* gx_next,
+                                                                    const float* __restrict__ gain, void* gs) {
+    constexpr int W = flat_width<IO>();
+    using Io = IoVec<IO, W>;
+    flat_pieces<W, typename Io::raw>(
+        pieces, F, step, gain, [&](int64_t e) { return Io::load(gx_next, e); },
+        [&](const typename Io::raw& r, const FlatGains<W>& g, int64_t e) {
+            float out[W];
+#pragma unroll
+            for (int j = 0; j < W; ++j) out[j] = g.g[j] * Io::get(r, j);
+            Io::store(gs, e, out);
+        });
+}
+
 }  // namespace snnlif
 
 namespace snnlif {

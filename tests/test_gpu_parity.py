@@ -201,7 +201,11 @@ def test_workload_stack(H):
 
 @pytest.mark.parametrize("io,spk", [("f32", "u8"), ("f32", "bits"), ("f32", "io"), ("bf16", "u8"),
                                     ("bf16", "bits"), ("bf16", "io")])
-@pytest.mark.parametrize("T,B,F", [(3, 2, 5), (9, 7, 100), (4, 3, 1024)])
+# Row-walking kernels (N not a multiple of the piece width, padded spike-bit rows) and the
+# flat ones: several workgroups with a partial last one, features not a multiple of the
+# piece width, fewer features than a piece holds.
+@pytest.mark.parametrize("T,B,F", [(3, 2, 5), (9, 7, 100), (4, 3, 1024), (5, 3, 4100), (7, 5, 1000),
+                                   (3, 65, 1088), (5, 40, 8), (6, 8, 2), (4, 4, 6)])
 def test_gain_glue(H, io, spk, T, B, F):
     torch = H.torch
     rng = np.random.default_rng(T * 100 + B + F)
@@ -227,6 +231,9 @@ def test_gain_glue(H, io, spk, T, B, F):
     ref, bound = H.oracle.gain_backward(gxn, np.abs(gxn), gain, B, F)
     rtol = H.parity.RTOL_BF16 if io == "bf16" else 1e-7
     assert np.all(np.abs(H.to_host_f32(gs) - ref) <= rtol * bound)
+    inplace = H.to_dev(gxn, io)                         # grad_s may be grad_x_next
+    H.native.snn_gain_grad_backward(cfg.c(), T, B, F, inplace, g, inplace)
+    assert torch.equal(inplace.view(torch.uint8), gs.view(torch.uint8))
 
 
 # Shapes that reach every lane/chunk plan of the library, run in full on the GPU and checked
