@@ -26,8 +26,18 @@ snn_status backward_entry(int reset, const Plan& p, const LifK& k, int64_t T, in
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
-            return launch(lif_backward_kernel<IO, R, Vc, Kc, Pc>, grid_for((N + Vc - 1) / Vc), s, k, T, N, x, sv,
-                          gs, gx, seg);
+            auto run = [&](auto blk, auto sync) {
+                constexpr int B = decltype(blk)::value;
+                constexpr bool S = decltype(sync)::value;
+                return launch_blk(lif_backward_kernel<IO, R, Vc, Kc, Pc, B, S>, grid_for((N + Vc - 1) / Vc, B), B, s,
+                                  k, T, N, x, sv, gs, gx, seg);
+            };
+            if constexpr (!Pc && Vc == 2) {
+                if (p.blkb == kSyncBlock)
+                    return p.syncb ? run(IntC<kSyncBlock>{}, std::true_type{})
+                                   : run(IntC<kSyncBlock>{}, std::false_type{});
+            }
+            return run(IntC<kBlock>{}, std::false_type{});
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});

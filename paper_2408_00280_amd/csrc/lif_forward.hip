@@ -22,17 +22,24 @@ snn_status forward_entry(int reset, const Plan& p, const LifK& k, int64_t T, int
                          hipStream_t s) {
     uint8_t* sp = static_cast<uint8_t*>(spikes);
     float* sv = static_cast<float*>(saved);
-    const dim3 g = grid_for(p.lanes);
     auto go = [&](auto rst) {
         return forward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
             constexpr bool Pc = decltype(PIPE)::value;
             constexpr int FB = forward_batch(IO, Vc, Kc, Pc);
-            return v_out ? launch(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, true, Pc>, g, s, k, T, N, x, sp,
-                                  p.row_bytes, sv, v_out, v_in, v_last)
-                         : launch(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, false, Pc>, g, s, k, T, N, x, sp,
-                                  p.row_bytes, sv, v_out, v_in, v_last);
+            auto run = [&](auto blk) {
+                constexpr int B = decltype(blk)::value;
+                const dim3 g = grid_for(p.lanes, B);
+                return v_out ? launch_blk(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, true, Pc, B>, g, B, s, k, T, N,
+                                          x, sp, p.row_bytes, sv, v_out, v_in, v_last)
+                             : launch_blk(lif_forward_kernel<IO, SPK, R, Vc, FB, Kc, false, Pc, B>, g, B, s, k, T, N,
+                                          x, sp, p.row_bytes, sv, v_out, v_in, v_last);
+            };
+            if constexpr (!Pc && Vc >= 2) {
+                if (p.blkf == kSyncBlock) return run(IntC<kSyncBlock>{});
+            }
+            return run(IntC<kBlock>{});
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});

@@ -48,6 +48,9 @@ struct Plan {
     int vb;
     int k;
     bool pipe;
+    int blkf;        // workgroup sizes of the dense forward and backward kernels
+    int blkb;
+    bool syncb;      // the backward's kSyncBlock workgroups meet at a barrier after each chunk
     int64_t lanes;   // lanes in the forward grid
     int64_t row_bytes;
 };
@@ -65,6 +68,17 @@ constexpr int kShortChunks[] = {4, 8, 16};
 
 // Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
 constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
+
+// Workgroup size for layers of several chunks that are not double-buffered.  Such a walk
+// over many rows loses bandwidth as the waves drift apart along it and their accesses of
+// the same moment spread over more DRAM pages; 16 waves that start together and meet at
+// a barrier after every chunk cover 8-16 KB of each row at once.  Measured against
+// 256-lane workgroups: forward -4% (bf16, T = 256) to -6.5% (fp32, T = 128 and 256);
+// fp32 backward -1.5% / -5% / -6.5% / -2.5% at T = 32 / 64 / 128 / 256 (N = 8.4M).  The
+// bf16 backward (32-step chunks, one such workgroup per CU) ran either 4% faster or 11%
+// slower from run to run with the barrier, and a steady 1.5-3% faster without it, so
+// there the workgroup takes no barrier.
+constexpr int kSyncBlock = 1024;
 
 inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
@@ -86,6 +100,10 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     }
     // bf16 forward: 8 neurons per lane (16-byte rows, whole spike bytes) on large layers
     p.vf = (c->io == SNN_IO_BF16 && N % 8 == 0 && N / 8 >= kFillLanes) ? 8 : p.vb;
+    const bool long_walk = !p.pipe && T > p.k;   // several chunks, not double-buffered
+    p.blkf = long_walk && p.vf >= 2 ? kSyncBlock : kBlock;   // the lane widths measured
+    p.blkb = long_walk && p.vb == 2 ? kSyncBlock : kBlock;
+    p.syncb = c->io == SNN_IO_F32;
     p.row_bytes = spike_row_bytes(c, N);
     const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
     p.lanes = (covered + p.vf - 1) / p.vf;
@@ -141,7 +159,7 @@ inline LifK kernel_consts(const snn_lif_cfg* c) {
     return k;
 }
 
-inline dim3 grid_for(int64_t lanes) { return dim3(unsigned((lanes + kBlock - 1) / kBlock)); }
+inline dim3 grid_for(int64_t lanes, int blk = kBlock) { return dim3(unsigned((lanes + blk - 1) / blk)); }
 
 template <typename Tuple, size_t... I>
 void fill_argv(Tuple& t, void** argv, std::index_sequence<I...>) {
@@ -151,13 +169,18 @@ void fill_argv(Tuple& t, void** argv, std::index_sequence<I...>) {
 // Launch through hipLaunchKernel so the runtime's verdict is returned directly and the
 // caller's sticky error state is left alone.
 template <typename... P, typename... A>
-snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
+snn_status launch_blk(void (*kernel)(P...), dim3 grid, int blk, hipStream_t stream, A... a) {
     static_assert(sizeof...(P) == sizeof...(A), "argument count");
     std::tuple<P...> args(a...);
     void* argv[sizeof...(P)];
     fill_argv(args, argv, std::index_sequence_for<P...>{});
-    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(kBlock), argv, 0, stream);
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(blk), argv, 0, stream);
     return e == hipSuccess ? SNN_OK : SNN_E_LAUNCH;
+}
+
+template <typename... P, typename... A>
+snn_status launch(void (*kernel)(P...), dim3 grid, hipStream_t stream, A... a) {
+    return launch_blk(kernel, grid, kBlock, stream, a...);
 }
 
 // Rows per load batch of the forward.  The forward never revisits a row, so it need not

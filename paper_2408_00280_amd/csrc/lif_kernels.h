@@ -430,7 +430,8 @@ __device__ __forceinline__ void forward_rows(const LifK& c, const In& in, const 
 // Segment state (a sequence split along time): v_in, if not null, is the membrane the
 // previous segment ended with, and the spike state entering the first step is v_in >= V_th;
 // v_last, if not null, receives the membrane after the last step.
-template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE, bool ALL, typename In>
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE, bool ALL, typename In,
+          bool SYNC = false>
 __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
                                               uint8_t* __restrict__ spikes, int64_t row_bytes,
                                               float* __restrict__ saved, float* __restrict__ v_out,
@@ -479,6 +480,7 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
         for (int64_t ch = 0; ch < n_full; ++ch) {
             load(a, ch);
             step(a, ch, maybe_last);
+            if constexpr (SYNC) __syncthreads();   // the workgroup's waves walk the rows in step
         }
     } else if (n_full > 0) {
         raw b[K];
@@ -517,21 +519,24 @@ __device__ __forceinline__ void forward_lanes(const LifK& c, const In& in, int64
 
 // Grid: one lane per V neurons over ceil(max(N, 8*row_bytes) / V) lanes.  Lanes at or beyond
 // N load nothing and report no spikes; they exist only to complete spike-bit words.
-template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE>
-__global__ __launch_bounds__(kBlock) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
-                                                             const void* __restrict__ x,
-                                                             uint8_t* __restrict__ spikes,
-                                                             int64_t row_bytes,
-                                                             float* __restrict__ saved,
-                                                             float* __restrict__ v_out,
-                                                             const float* __restrict__ v_in,
-                                                             float* __restrict__ v_last) {
-    const int64_t first = xcd_contiguous_block() * kBlock * V;
+// BLK: the workgroup size; above kBlock (layers of several chunks, not double-buffered)
+// the waves of a workgroup that lies wholly inside N meet at a barrier after every chunk.
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE, int BLK = kBlock>
+__global__ __launch_bounds__(BLK) void lif_forward_kernel(LifK c, int64_t T, int64_t N,
+                                                          const void* __restrict__ x,
+                                                          uint8_t* __restrict__ spikes,
+                                                          int64_t row_bytes,
+                                                          float* __restrict__ saved,
+                                                          float* __restrict__ v_out,
+                                                          const float* __restrict__ v_in,
+                                                          float* __restrict__ v_last) {
+    static_assert(BLK == kBlock || !PIPE, "barriers only in the single-buffered chunk loop");
+    const int64_t first = xcd_contiguous_block() * BLK * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
     const DenseIn<IO, V> in{x};
-    if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
-                                                              v_in, v_last);
+    if (first + BLK * V <= N)
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, true, DenseIn<IO, V>, (BLK > kBlock)>(
+            c, in, T, N, n0, spikes, row_bytes, saved, v_out, v_in, v_last);
     else
         forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                                v_in, v_last);
@@ -663,7 +668,7 @@ __device__ __forceinline__ void backward_chunk(const LifK& c, const In& in, cons
 }
 
 // Chunks are processed last-first: the short tail chunk (if any), then the full chunks.
-template <int IO, int RESET, int V, int K, bool PIPE, bool GAIN, typename In>
+template <int IO, int RESET, int V, int K, bool PIPE, bool GAIN, typename In, bool SYNC = false>
 __device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int64_t T, int64_t N, int64_t n0,
                                                const float* __restrict__ saved, const void* gs, void* gx,
                                                const BwdSeg& seg) {
@@ -695,6 +700,7 @@ __device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int6
         for (int64_t ch = n_full - 1; ch >= 0; --ch) {
             load(a, ch);
             step(a, ch);
+            if constexpr (SYNC) __syncthreads();   // the workgroup's waves walk the rows in step
         }
     } else if (n_full > 0) {
         Chunk b;
@@ -724,15 +730,23 @@ __device__ __forceinline__ void backward_lanes(const LifK& c, const In& in, int6
     if (seg.g_out != nullptr) store_f32<V>(seg.g_out + n0, g);
 }
 
-template <int IO, int RESET, int V, int K, bool PIPE>
-__global__ __launch_bounds__(kBlock) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
-                                                              const void* __restrict__ x,
-                                                              const float* __restrict__ saved,
-                                                              const void* gs, void* gx, BwdSeg seg) {
-    const int64_t first = xcd_contiguous_block() * kBlock * V;
+// BLK: the workgroup size.  SYNC: its waves meet at a barrier after every chunk (only in
+// a workgroup wholly inside N; one that is not drops its lanes beyond N).
+template <int IO, int RESET, int V, int K, bool PIPE, int BLK = kBlock, bool SYNC = false>
+__global__ __launch_bounds__(BLK) void lif_backward_kernel(LifK c, int64_t T, int64_t N,
+                                                           const void* __restrict__ x,
+                                                           const float* __restrict__ saved,
+                                                           const void* gs, void* gx, BwdSeg seg) {
+    static_assert(!SYNC || !PIPE, "barriers only in the single-buffered chunk loop");
+    const int64_t first = xcd_contiguous_block() * BLK * V;
     const int64_t n0 = first + int64_t(threadIdx.x) * V;
-    if (first + kBlock * V > N && n0 >= N) return;
-    backward_lanes<IO, RESET, V, K, PIPE, false>(c, DenseIn<IO, V>{x}, T, N, n0, saved, gs, gx, seg);
+    const DenseIn<IO, V> in{x};
+    if (first + BLK * V <= N) {
+        backward_lanes<IO, RESET, V, K, PIPE, false, DenseIn<IO, V>, SYNC>(c, in, T, N, n0, saved, gs, gx, seg);
+        return;
+    }
+    if (n0 >= N) return;
+    backward_lanes<IO, RESET, V, K, PIPE, false>(c, in, T, N, n0, saved, gs, gx, seg);
 }
 
 // Backward of the gain-fed layer: recomputes from the previous layer's spikes and writes

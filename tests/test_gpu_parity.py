@@ -241,11 +241,14 @@ def test_gain_glue(H, io, spk, T, B, F):
 # layers (T <= 16) of at least 2^20 neurons; the bf16 forward takes 8 per lane from 2^21.
 # Chunks: 16 steps (32 at 1 per lane, and for bf16 layers not double-buffered, whose forward
 # loads them 16 rows at a time), double-buffered below 2^20 lanes, a short tail chunk when
-# K does not divide T, and 4/8/16-step single chunks for short layers.
+# K does not divide T, and 4/8/16-step single chunks for short layers.  Layers of several
+# chunks that are not double-buffered run in 1024-lane workgroups with a barrier per chunk.
 PLAN_SHAPES = [
     (16, 1 << 20),          # one chunk (fp32 2 per lane, bf16 4)
     (40, (1 << 20) + 4),    # 2 per lane, double-buffered 16-step chunks, tail
     (40, 1 << 22),          # not double-buffered: fp32 16-step, bf16 32-step chunks (forward 8 per lane)
+    (40, (1 << 22) + 6),    # the same at 2 per lane with a partial last workgroup
+    (72, (1 << 20) + 1),    # 1 per lane, not double-buffered 32-step chunks, tail
     (16, 524290),           # 2 per lane, one chunk
     (40, 600002),           # 2 per lane, double-buffered, tail
     (40, 262145),           # 1 per lane (odd N), double-buffered 32-step chunks, tail
