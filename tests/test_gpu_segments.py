@@ -31,6 +31,7 @@ SPLITS = [
     (100, 70001, [50, 50]),
     (40, (1 << 20) + 4, [8, 9, 23]),
     (48, 1 << 21, [16, 32]),
+    (80, 1 << 21, [40, 40]),    # multi-chunk segments in 1024-lane workgroups (bf16 too)
 ]
 
 
