@@ -53,12 +53,20 @@ def bytes_per_nts(w):
             "lif_stack_forward": e + s, "lif_stack_backward": 3 * e}
 
 
-def source_hash() -> str:
-    """Hash of the kernel sources (every file under csrc/, in name order)."""
+def code_of(text: str) -> str:
+    """C/C++ source without its comments, whitespace runs collapsed: what the compiler sees
+    of it, so that editing a comment does not make measurements of the code look stale."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def source_hash(src_dir: str = KERNEL_SRC_DIR) -> str:
+    """Hash of the kernel code (every file under csrc/, in name order, comments removed)."""
     h = hashlib.sha256()
-    for name in sorted(os.listdir(KERNEL_SRC_DIR)):
-        with open(os.path.join(KERNEL_SRC_DIR, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+    for name in sorted(os.listdir(src_dir)):
+        with open(os.path.join(src_dir, name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + code_of(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -69,10 +69,11 @@ constexpr int kShortChunks[] = {4, 8, 16};
 // Lanes that fill the chip with 16 waves per CU (256 CUs x 16 x 64).
 constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 
-// Workgroup size for layers of several chunks that are not double-buffered.  Such a walk
-// over many rows loses bandwidth as the waves drift apart along it and their accesses of
-// the same moment spread over more DRAM pages; 16 waves that start together and meet at
-// a barrier after every chunk cover 8-16 KB of each row at once.  Measured against
+// Workgroup size for layers of several chunks that are not double-buffered.  Rows lie
+// 16-32 MiB apart, each in its own 2 MiB page, and a wave uses a few hundred bytes of each;
+// as waves drift apart along a long walk, the pages in use at once outgrow the per-CU
+// address-translation cache.  16 waves that start together and meet at a barrier after
+// every chunk share the translations of the same rows' pages.  Measured against
 // 256-lane workgroups: forward -4% (bf16, T = 256) to -6.5% (fp32, T = 128 and 256);
 // fp32 backward -1.5% / -5% / -6.5% / -2.5% at T = 32 / 64 / 128 / 256 (N = 8.4M).  The
 // bf16 backward (32-step chunks, one such workgroup per CU) ran either 4% faster or 11%

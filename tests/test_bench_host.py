@@ -55,3 +55,14 @@ def test_committed_summaries_parse():
         text = open(os.path.join(bench.PROFILES, n)).read()
         assert "source_sha256_16:" in text and "traffic_bytes_per_launch:" in text, n
         assert "rocprofv3 --pmc FETCH_SIZE" in text and "rocprofv3 --pmc WRITE_SIZE" in text, n
+
+
+def test_source_hash_ignores_comments_only(tmp_path):
+    """The hash that ties profiles to kernel code changes with the code, not with comments."""
+    src = tmp_path / "k.hip"
+    src.write_text("// leading note\nint f(int a) {  /* old */ return a + 1; }  // tail\n")
+    before = bench.source_hash(str(tmp_path))
+    src.write_text("// a reworded note\n/* a new block\n   comment */\nint f(int a) {\n    return a + 1;\n}\n")
+    assert bench.source_hash(str(tmp_path)) == before
+    src.write_text("int f(int a) { return a + 2; }\n")
+    assert bench.source_hash(str(tmp_path)) != before
