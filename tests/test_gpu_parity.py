@@ -248,6 +248,7 @@ PLAN_SHAPES = [
     (40, (1 << 20) + 4),    # 2 per lane, double-buffered 16-step chunks, tail
     (40, 1 << 22),          # not double-buffered: fp32 16-step, bf16 32-step chunks (forward 8 per lane)
     (40, (1 << 22) + 6),    # the same at 2 per lane with a partial last workgroup
+    (40, (1 << 22) + 8),    # bf16 forward 8 per lane with a partial last workgroup
     (72, (1 << 20) + 1),    # 1 per lane, not double-buffered 32-step chunks, tail
     (16, 524290),           # 2 per lane, one chunk
     (40, 600002),           # 2 per lane, double-buffered, tail
