@@ -9,10 +9,15 @@ dominant kernel (the backward) from HIP events recorded on the launch stream aro
 launch, and the CPU oracle's throughput on the host as a baseline.
 
     python bench.py [--steps K] [--warmup W] [--workload conv|single|long|stack|large]
-                    [--T T] [--fused-stack] [--no-cpu-baseline] [--with-copy]
+                    [--T T] [--fused-stack | --depth-stack] [--graph-trials N]
+                    [--no-cpu-baseline] [--with-copy] [--compare-serial [--Ts ...]]
 
 --fused-stack runs a stack's layers after the first fed straight from the previous
-layer's spikes through the gain (no stored input current or dL/dx between layers).
+layer's spikes through the gain (no stored input current or dL/dx between layers);
+--depth-stack runs the whole stack as one kernel per direction.  --graph-trials (single
+workload) adds independent forward+backward trials replayed from one HIP graph as a
+separate figure; --with-copy adds the 1 GiB copy that calibrates the traffic counters;
+--compare-serial times the fused layer against the per-step serial baseline over T.
 
 Workloads whose buffers are smaller than the 256 MB Infinity Cache rotate over several
 independent buffer sets (about 1 GiB in total), one set per step, so that a step does not
