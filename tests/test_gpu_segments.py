@@ -134,3 +134,55 @@ def test_segment_errors(H):
     nat.snn_lif_backward_seg(cfg.c(), 0, N, None, None, None, None, None, None, keep)
     torch.cuda.synchronize()
     assert bool((keep == 7.0).all())
+
+
+def _random_splits():
+    """Seeded random cases: layer sizes on every plan (small, double-buffered, 1024-lane
+    workgroups), 2-4 segments of random lengths, random hyper-parameters and formats."""
+    rng = np.random.default_rng(20240803)
+    sizes = [int(rng.integers(1, 5000)), int(rng.integers(60000, 80000)), int(rng.integers(500000, 700000)),
+             2 * int(rng.integers(1 << 20, (1 << 21) + 500))]   # even: 2 neurons per lane, 1024-lane workgroups
+    out = []
+    for i in range(12):
+        T = int(rng.integers(2, 91))
+        N = sizes[i % len(sizes)]
+        n_seg = int(rng.integers(2, min(4, T) + 1))
+        cuts = np.sort(rng.choice(np.arange(1, T), size=n_seg - 1, replace=False))
+        lens = [int(v) for v in np.diff(np.r_[0, cuts, T])]
+        p = (float(rng.uniform(0, 1)), float(rng.uniform(0.2, 2.0)), float(rng.choice([0.0, rng.uniform(-0.5, 0.5)])),
+             str(rng.choice(["hard", "soft"])))
+        out.append((i, T, N, lens, p, str(rng.choice(["f32", "bf16"])), str(rng.choice(["u8", "bits", "io"]))))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_splits(), ids=lambda c: f"rnd{c[0]}")
+def test_random_segments_equal_whole(H, case):
+    """Segments with the state handoff reproduce the single run bit for bit (the single run
+    itself is checked against the oracle by the other parity tests)."""
+    torch = H.torch
+    i, T, N, lens, (decay, v_th, v_reset, reset), io, spk = case
+    w = H.W.custom(f"rseg{i}", T, N, H.W.LifParams(decay, v_th, v_reset=v_reset, reset=reset), seed=700 + i, io=io,
+                   spk=spk, x_dist=("normal", 0.5 * v_th, 0.5 * v_th + 0.2))
+    cfg = H.cfg_of(w)
+    x, gs = H.upload_rows(w, "x"), H.upload_rows(w, "gs")
+    spikes, saved, v = H.layer.forward(cfg, x, v_out=True)
+    gx = H.layer.backward(cfg, x, saved, gs)
+    bounds = np.cumsum([0] + lens)
+    states, v_in = [], None
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        xs = x[a:b].clone()
+        v_last = torch.empty(N, dtype=torch.float32, device=H.DEV)
+        s_seg, sv_seg, v_seg = H.layer.forward(cfg, xs, v_out=True, v_in=v_in, v_last=v_last)
+        assert torch.equal(s_seg, spikes[a:b]) and torch.equal(v_seg, v[a:b]), f"segment [{a}, {b}) of {lens}"
+        states.append((a, b, xs, sv_seg, v_in))
+        v_in = v_last
+    g_in = None
+    for a, b, xs, sv_seg, vi in reversed(states):
+        g_out = torch.empty(N, dtype=torch.float32, device=H.DEV)
+        gx_seg = H.layer.backward(cfg, xs, sv_seg, gs[a:b].clone(), v_in=vi, g_in=g_in, g_out=g_out)
+        assert torch.equal(gx_seg.view(torch.uint8), gx[a:b].view(torch.uint8)), f"dL/dx of [{a}, {b}) of {lens}"
+        g_in = g_out
+    torch.cuda.synchronize()
+    H.say(f"random segments {i}: T={T} N={N} {lens} {reset} {io} {spk}: equal")
+    del x, gs, spikes, saved, v, gx, states
+    torch.cuda.empty_cache()
