@@ -48,12 +48,13 @@ def _spikes(H, t, N, spk):
     return H.parity.unpack_spikes(H.to_host_f32(t) if spk == "io" else t.cpu().numpy(), N, spk)
 
 
-def _run(H, T, B, F, L, reset, io, spk, seed, n_sample=None, inplace=False):
+def _run(H, T, B, F, L, reset, io, spk, seed, n_sample=None, inplace=False, p=None):
     torch = H.torch
     from paper_2408_00280_amd import stack
     N = B * F
-    p = H.W.LifParams(0.5, 1.0, reset=reset)
-    w = H.W.custom(f"depth{T}x{N}", T, N, p, seed=seed, io=io, spk=spk, x_dist=("normal", 0.5, 0.6))
+    x_dist = ("normal", 0.5, 0.6) if p is None else ("normal", 0.5 * p.v_th, 0.6 * abs(p.v_th) + 0.1)
+    p = p or H.W.LifParams(0.5, 1.0, reset=reset)
+    w = H.W.custom(f"depth{T}x{N}", T, N, p, seed=seed, io=io, spk=spk, x_dist=x_dist)
     cfg = H.cfg_of(w)
     rng = np.random.default_rng(seed)
     gains = [rng.uniform(-0.3, 1.8, size=F).astype(np.float32) for _ in range(L - 1)]
@@ -151,3 +152,27 @@ def test_depth_stack_errors(H):
     assert nat.snn_lif_stack_saved_bytes(cfg.c(), 2, 16, B * F) == 0
     nat.snn_lif_stack_forward(cfg.c(), 3, 0, B, F, None, None, None, None, None)
     torch.cuda.synchronize()
+
+
+def _random_cases():
+    rng = np.random.default_rng(20240804)
+    out = []
+    for i in range(16):
+        T = int(rng.integers(1, 70))
+        B = int(rng.integers(1, 9))
+        F = int(rng.integers(1, 3000))
+        L = int(rng.choice([2, 3]))
+        p = (float(rng.uniform(0, 1)), float(rng.uniform(0.2, 2.0)), float(rng.choice([0.0, rng.uniform(-0.5, 0.5)])),
+             float(rng.uniform(1.0, 8.0)), str(rng.choice(["hard", "soft"])))
+        out.append((i, T, B, F, L, p, str(rng.choice(["f32", "bf16"])), str(rng.choice(["u8", "bits", "io"]))))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: f"rnd{c[0]}")
+def test_depth_stack_random(H, case):
+    """Seeded random depth, shapes, formats and hyper-parameters, against the oracle run
+    layer by layer (and, for fp32, the gain-fused schedule bit for bit)."""
+    i, T, B, F, L, (decay, v_th, v_reset, alpha, reset), io, spk = case
+    p = H.W.LifParams(decay, v_th, v_reset=v_reset, alpha=alpha, reset=reset)
+    rep = _run(H, T, B, F, L, reset, io, spk, seed=1000 + i, p=p)
+    assert rep.ok(), f"{case}: {rep}"
