@@ -165,3 +165,20 @@ def test_c_client_links():
     assert "not found" not in out
     for lib in ("libsnnlif.so", "liboracle.so", "libsynth.so", "libamdhip64"):
         assert lib in out, lib
+
+
+@pytest.mark.parametrize("compiler,flags,ext", [("gcc", ["-std=c99"], "c"), ("g++", ["-std=c++11"], "cc")])
+def test_header_is_plain_c_and_cxx(tmp_path, compiler, flags, ext):
+    """include/snn_lif.h compiles on its own, warning-free and pedantic, as C99 and as C++11
+    (no HIP or torch types in the interface)."""
+    import shutil
+    import subprocess
+    if shutil.which(compiler) is None:
+        pytest.skip(f"{compiler} not available")
+    src = tmp_path / f"use.{ext}"
+    src.write_text('#include "snn_lif.h"\n'
+                   "snn_status probe(const snn_lif_cfg *c, size_t *b) { return snn_lif_saved_bytes(c, 4, 64, b); }\n")
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    r = subprocess.run([compiler, *flags, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-I", inc, str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
