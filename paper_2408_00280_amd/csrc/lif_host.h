@@ -76,10 +76,13 @@ constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 // every chunk share the translations of the same rows' pages.  Measured against
 // 256-lane workgroups: forward -4% (bf16, T = 256) to -6.5% (fp32, T = 128 and 256);
 // fp32 backward -1.5% / -5% / -6.5% / -2.5% at T = 32 / 64 / 128 / 256 (N = 8.4M).  The
-// bf16 backward (32-step chunks, one such workgroup per CU) ran either 4% faster or 11%
-// slower from run to run with the barrier, and a steady 1.5-3% faster without it, so
-// there the workgroup takes no barrier.
+// bf16 backward (32-step chunks, one such workgroup per CU) with the barrier is 1.3-2.6%
+// faster than without it at T = 64 / 96 / 128 / 192 in every run (21 runs, five boxes),
+// but at T = 256 it ran 13% slower in about half the runs, so it takes the barrier only
+// for layers of at most kSyncBf16Chunks chunks; without one it is a steady 1.5-3% faster
+// than 256-lane workgroups.
 constexpr int kSyncBlock = 1024;
+constexpr int kSyncBf16Chunks = 6;
 
 inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     Plan p;
@@ -104,7 +107,7 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     const bool long_walk = !p.pipe && T > p.k;   // several chunks, not double-buffered
     p.blkf = long_walk && p.vf >= 2 ? kSyncBlock : kBlock;   // the lane widths measured
     p.blkb = long_walk && p.vb == 2 ? kSyncBlock : kBlock;
-    p.syncb = c->io == SNN_IO_F32;
+    p.syncb = c->io == SNN_IO_F32 || (T + p.k - 1) / p.k <= kSyncBf16Chunks;
     p.row_bytes = spike_row_bytes(c, N);
     const int64_t covered = c->spk == SNN_SPK_BITS ? p.row_bytes * 8 : N;
     p.lanes = (covered + p.vf - 1) / p.vf;
