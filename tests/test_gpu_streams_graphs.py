@@ -27,6 +27,8 @@ CASES = [
     (20, 1 << 21, "soft", "bf16", "bits"),
     (4, 65536, "hard", "f32", "bits"),
     (33, 4096, "soft", "bf16", "io"),
+    (72, 1 << 21, "hard", "f32", "u8"),       # several chunks in 1024-lane workgroups with barriers
+    (80, 1 << 21, "soft", "bf16", "bits"),    # the same in bf16 (8-neuron forward lanes)
 ]
 
 
