@@ -81,6 +81,9 @@ constexpr int64_t kFillLanes = int64_t(256) * 16 * 64;
 // but at T = 256 it ran 13% slower in about half the runs, so it takes the barrier only
 // for layers of at most kSyncBf16Chunks chunks; without one it is a steady 1.5-3% faster
 // than 256-lane workgroups.
+// A 1024-lane workgroup allows 128 VGPRs per lane: the 8-neuron bf16 forward with spikes
+// in the I/O dtype needs about 150 and spills some 40, yet still ran 2% / 5% faster than
+// the spill-free 256-lane kernel at T = 64 / 256 (N = 2^24), so it keeps these workgroups.
 constexpr int kSyncBlock = 1024;
 constexpr int kSyncBf16Chunks = 6;
 
