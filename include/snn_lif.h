@@ -133,9 +133,11 @@ snn_status snn_lif_backward_seg(const snn_lif_cfg *cfg, int64_t T, int64_t N, co
 /* Stand-in for the ANN operator between stacked LIF layers (not part of the paper's
  * method): a per-feature gain, N = B*F neurons per step, neuron (b, f) at b*F + f.
  *   forward:  x_next[t][b][f] = gain[f] * y[t][b][f]   (spikes in cfg->spk format,
- *             x_next in cfg->io dtype, product in fp32 then rounded to the io dtype);
- *   backward: grad_s[t][b][f] = gain[f] * grad_x_next[t][b][f]   (io dtype in and out;
- *             may be the same buffer).
+ *             x_next in cfg->io dtype, product in fp32 then rounded to the io dtype; y is
+ *             0 or 1, so this is gain[f] rounded to the io dtype, times y);
+ *   backward: grad_s[t][b][f] = g[f] * grad_x_next[t][b][f], g[f] = gain[f] rounded to the
+ *             io dtype as the forward applies it (io dtype in and out; product in fp32,
+ *             rounded once; may be the same buffer).
  * gain is a device float32 [F] array. */
 snn_status snn_gain_spikes_forward(const snn_lif_cfg *cfg, int64_t T, int64_t B, int64_t F,
                                    const void *spikes, const float *gain, void *x_next,
@@ -158,9 +160,10 @@ snn_status snn_gain_grad_backward(const snn_lif_cfg *cfg, int64_t T, int64_t B, 
  * forward_gain: spikes, saved, v_out as in snn_lif_forward.
  * backward_gain: spikes_in, gain, saved exactly as in the matching forward_gain; grad_s
  *              [T][N] io: dL/dy of this layer; grad_s_in [T][N] io out: dL/d spikes_in =
- *              gain[f] * dL/dx, formed in fp32 and rounded once to the io dtype (the
- *              unfused pair rounds dL/dx first, so bf16 results may differ there in the
- *              last bit).  grad_s_in may be the same buffer as grad_s; no other overlap.
+ *              g[f] * dL/dx with g[f] = gain[f] rounded to cfg->io (the factor the input
+ *              current was formed with), formed in fp32 and rounded once to the io dtype
+ *              (the unfused pair rounds dL/dx first, so bf16 results may differ there in
+ *              the last bit).  grad_s_in may be the same buffer as grad_s; no other overlap.
  * x is never materialised: per (t, n) the forward reads 1 B (u8) or 1/8 B (bits) of input
  * instead of 4 B or 2 B (with I/O-dtype spikes it saves the glue kernel's write and read of
  * x). */
@@ -189,8 +192,8 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg *cfg, int64_t T, int64_t B, i
  *   v_out      NULLABLE [L][T][N] float32 out: every layer's membranes (tests).
  * backward: x, gains, saved exactly as in the forward; grad_s [T][N] io: dL/dy of the last
  * layer; grad_x [T][N] io out: dL/dx of layer 0 (may be the same buffer as grad_s).  The
- * gradient handed from layer l down to layer l-1, gain dL/dx_l, stays in fp32 (the
- * layer-by-layer run stores it in the io dtype).  Other L: SNN_E_UNSUPPORTED. */
+ * gradient handed from layer l down to layer l-1, g dL/dx_l with g the gain rounded to
+ * cfg->io, stays in fp32 (the layer-by-layer run stores it in the io dtype).  Other L: SNN_E_UNSUPPORTED. */
 snn_status snn_lif_stack_saved_bytes(const snn_lif_cfg *cfg, int32_t L, int64_t T, int64_t N,
                                      size_t *bytes);
 snn_status snn_lif_stack_forward(const snn_lif_cfg *cfg, int32_t L, int64_t T, int64_t B, int64_t F,

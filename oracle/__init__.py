@@ -45,12 +45,16 @@ def load(path: str = _LIB_PATH):
     lib = ctypes.CDLL(path)
     P, i64, vp = ctypes.POINTER(_Params), ctypes.c_int64, ctypes.c_void_p
     lib.lif_oracle_forward.argtypes = [P, i64, i64, vp, vp, vp, vp, vp]
-    lib.lif_oracle_backward.argtypes = [P, i64, i64, vp, vp, vp, vp, vp, vp, vp]
+    ci = ctypes.c_int
+    lib.lif_oracle_backward.argtypes = [P, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.lif_oracle_gain_forward.argtypes = [i64, i64, i64, vp, vp, vp]
-    lib.lif_oracle_gain_backward.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp]
+    lib.lif_oracle_gain_backward.argtypes = [i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
+    lib.lif_oracle_stack_forward.argtypes = [P, ci, i64, i64, i64, vp, vp, vp, vp, vp]
+    lib.lif_oracle_stack_backward.argtypes = [P, ci, i64, i64, i64, vp, vp, vp, vp, ci, vp, vp, vp]
     for f in ("lif_oracle_forward", "lif_oracle_backward", "lif_oracle_gain_forward",
-              "lif_oracle_gain_backward"):
+              "lif_oracle_gain_backward", "lif_oracle_stack_forward"):
         getattr(lib, f).restype = None
+    lib.lif_oracle_stack_backward.restype = ctypes.c_int
     if path == _LIB_PATH:
         _lib = lib
     return lib
@@ -100,22 +104,48 @@ def forward(p: Params, x, v_init=None, y_init=None, lib=None):
     return y, v
 
 
-def backward(p: Params, v, y, gy, gy_mag=None, g_next=None, lib=None):
-    """Eq. (3) in reverse time, fp64.  Returns (gx float64 [T][N], bound float64 [T][N])."""
+@dataclass
+class Grad:
+    """dL/dx from the oracle's backward (fp64) with its two running error budgets:
+    `err` scales with the evaluation's per-operation relative error, `rnd` with the unit
+    roundoff of lower-precision copies of dL/dy that fed it (see lif_oracle.h)."""
+    g: np.ndarray
+    err: np.ndarray
+    rnd: np.ndarray
+
+    def sel(self, idx) -> "Grad":
+        """The same index applied to all three arrays."""
+        return Grad(self.g[idx], self.err[idx], self.rnd[idx])
+
+    @staticmethod
+    def exact(g) -> "Grad":
+        """An input known exactly (both budgets zero)."""
+        g = _c64(g)
+        return Grad(g, np.zeros_like(g), np.zeros_like(g))
+
+
+def backward(p: Params, v, y, gy, gy_err=None, gy_rnd=None, g_next=None, lib=None) -> Grad:
+    """Eq. (3) in reverse time, fp64, with its error budgets (float64 [T][N] each).
+    gy_err / gy_rnd: budgets of gy when an earlier computation produced it (None: exact)."""
     lib = lib or load()
     v = _c32(v)
     T, N = v.shape
     y = np.ascontiguousarray(y, dtype=np.uint8)
     gy = _c64(gy)
-    gy_mag = np.abs(gy) if gy_mag is None else _c64(gy_mag)
+    ge = None if gy_err is None else _c64(gy_err)
+    gr = None if gy_rnd is None else _c64(gy_rnd)
     gn = None if g_next is None else _c64(g_next)
-    assert y.shape == v.shape == gy.shape == gy_mag.shape
+    assert y.shape == v.shape == gy.shape
+    assert ge is None or ge.shape == gy.shape
+    assert gr is None or gr.shape == gy.shape
+    assert gn is None or gn.shape == (N,)
     gx = np.empty((T, N), dtype=np.float64)
-    gm = np.empty((T, N), dtype=np.float64)
+    err = np.empty((T, N), dtype=np.float64)
+    rnd = np.empty((T, N), dtype=np.float64)
     pc = p._c()
-    lib.lif_oracle_backward(ctypes.byref(pc), T, N, _ptr(v), _ptr(y), _ptr(gy), _ptr(gy_mag),
-                            _ptr(gn), _ptr(gx), _ptr(gm))
-    return gx, gm
+    lib.lif_oracle_backward(ctypes.byref(pc), T, N, _ptr(v), _ptr(y), _ptr(gy), _ptr(ge), _ptr(gr),
+                            _ptr(gn), _ptr(gx), _ptr(err), _ptr(rnd))
+    return Grad(gx, err, rnd)
 
 
 def gain_forward(y, gain, B: int, F: int, lib=None):
@@ -125,44 +155,66 @@ def gain_forward(y, gain, B: int, F: int, lib=None):
     T = y.shape[0]
     assert y.size == T * B * F
     g = _c32(gain)
+    assert g.shape == (F,)
     out = np.empty((T, B * F), dtype=np.float32)
     lib.lif_oracle_gain_forward(T, B, F, _ptr(y), _ptr(g), _ptr(out))
     return out
 
 
-def gain_backward(gx_next, gx_next_mag, gain, B: int, F: int, lib=None):
-    """gy[t][b][f] = gain[f] * gx_next[t][b][f] (fp64) and its bound."""
+def gain_backward(gx_next: Grad, gain, B: int, F: int, lib=None) -> Grad:
+    """gy[t][b][f] = gain[f] * gx_next[t][b][f] (fp64), budgets scaled by |gain[f]|."""
     lib = lib or load()
-    gx_next = _c64(gx_next)
-    gx_next_mag = _c64(gx_next_mag)
-    T = gx_next.shape[0]
+    a, e, r = _c64(gx_next.g), _c64(gx_next.err), _c64(gx_next.rnd)
+    T = a.shape[0]
+    assert a.size == T * B * F and e.shape == a.shape and r.shape == a.shape
     g = _c32(gain)
-    gy = np.empty((T, B * F), dtype=np.float64)
-    gm = np.empty((T, B * F), dtype=np.float64)
-    lib.lif_oracle_gain_backward(T, B, F, _ptr(gx_next), _ptr(gx_next_mag), _ptr(g), _ptr(gy), _ptr(gm))
-    return gy, gm
+    assert g.shape == (F,)
+    out = [np.empty((T, B * F), dtype=np.float64) for _ in range(3)]
+    lib.lif_oracle_gain_backward(T, B, F, _ptr(a), _ptr(e), _ptr(r), _ptr(g), *(_ptr(o) for o in out))
+    return Grad(*out)
+
+
+def _gains(gains, L: int, F: int):
+    g = _c32(np.reshape(gains, (L - 1, F)) if L > 1 else np.zeros((0, F)))
+    return np.ascontiguousarray(g)
 
 
 def stack_forward(p: Params, x1, gains, B: int, F: int, lib=None):
-    """L stacked layers, layer l+1 fed gains[l][f] * spikes of layer l.
-    Returns per-layer lists (xs, ys, vs)."""
-    xs, ys, vs = [_c32(x1)], [], []
-    for l in range(len(gains) + 1):
-        y, v = forward(p, xs[l], lib=lib)
-        ys.append(y)
-        vs.append(v)
-        if l < len(gains):
-            xs.append(gain_forward(y, gains[l], B, F, lib=lib))
-    return xs, ys, vs
+    """L = len(gains) + 1 stacked layers, layer l+1 fed gains[l][f] * spikes of layer l.
+    Returns per-layer lists (xs, ys, vs), layer 0 first."""
+    lib = lib or load()
+    x1 = _c32(x1)
+    T = x1.shape[0]
+    L = len(gains) + 1
+    assert x1.size == T * B * F
+    g = _gains(gains, L, F)
+    xs = np.empty((L, T, B * F), dtype=np.float32)
+    ys = np.empty((L, T, B * F), dtype=np.uint8)
+    vs = np.empty((L, T, B * F), dtype=np.float32)
+    pc = p._c()
+    lib.lif_oracle_stack_forward(ctypes.byref(pc), L, T, B, F, _ptr(x1), _ptr(g), _ptr(xs), _ptr(ys), _ptr(vs))
+    return list(xs), list(ys), list(vs)
 
 
-def stack_backward(p: Params, ys, vs, gy_last, gains, B: int, F: int, lib=None):
-    """Backward through the stack.  Returns per-layer lists (gxs, bounds), layer 0 first."""
+def stack_backward(p: Params, ys, vs, gy_last, gains, B: int, F: int, rounded_handoff: bool = False,
+                   lib=None) -> list:
+    """Backward through the stack from the last layer's dL/dy.  Returns a list of Grad,
+    dL/dx of every layer, layer 0 first.  rounded_handoff: the gradient passed down between
+    layers is stored in a lower precision (bf16 tensors between autograd layers)."""
+    lib = lib or load()
     L = len(ys)
-    gxs, gms = [None] * L, [None] * L
-    gy, gym = _c64(gy_last), np.abs(_c64(gy_last))
-    for l in range(L - 1, -1, -1):
-        gxs[l], gms[l] = backward(p, vs[l], ys[l], gy, gym, lib=lib)
-        if l > 0:
-            gy, gym = gain_backward(gxs[l], gms[l], gains[l - 1], B, F, lib=lib)
-    return gxs, gms
+    assert len(vs) == L and len(gains) == L - 1
+    y = np.ascontiguousarray(np.stack(ys), dtype=np.uint8)
+    v = _c32(np.stack(vs))
+    _, T, N = v.shape
+    assert N == B * F
+    gy = _c64(gy_last)
+    assert gy.shape == (T, N)
+    g = _gains(gains, L, F)
+    out = [np.empty((L, T, N), dtype=np.float64) for _ in range(3)]
+    pc = p._c()
+    rc = lib.lif_oracle_stack_backward(ctypes.byref(pc), L, T, B, F, _ptr(v), _ptr(y), _ptr(g), _ptr(gy),
+                                       int(rounded_handoff), *(_ptr(o) for o in out))
+    if rc != 0:
+        raise MemoryError("lif_oracle_stack_backward: out of memory")
+    return [Grad(out[0][l], out[1][l], out[2][l]) for l in range(L)]

@@ -65,8 +65,9 @@ class LIFLayer(torch.nn.Module):
 
 class FusedGainLIF(torch.autograd.Function):
     """A LIF layer fed by the previous layer's spikes through a fixed per-feature gain:
-    input current gain[f] * spikes_in[t, ..., f], formed inside the fused kernels.  The
-    backward returns dL/d spikes_in = gain[f] * dL/dx; the gain gets no gradient."""
+    input current gain[f] * spikes_in[t, ..., f], formed inside the fused kernels (the gain
+    rounded to the I/O dtype first).  The backward returns dL/d spikes_in = gain[f] * dL/dx
+    with the same rounded gain; the gain gets no gradient."""
 
     @staticmethod
     def forward(ctx, spikes_in: torch.Tensor, gain: torch.Tensor, cfg: layer.LifConfig):

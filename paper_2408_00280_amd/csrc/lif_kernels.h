@@ -104,6 +104,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// A float rounded to the I/O dtype (to nearest even for bf16), as a float.
+template <int IO>
+__device__ __forceinline__ float io_round(float f) {
+    if constexpr (IO == SNN_IO_BF16) return bf16_lo(pack_bf16x2(f, 0.0f));
+    else return f;
+}
+
 template <>
 struct IoVec<SNN_IO_BF16, 8> {
     using raw = u32x4_t;
@@ -342,7 +349,8 @@ __device__ __forceinline__ void load_f32(const float* p, float (&f)[V]) {
 //   GainSpikeIn -- x[t][b][f] = gain[f] * spikes_in[t][b][f], read straight from the previous
 //                  layer's spikes in any of the spike formats (a stack fused across its
 //                  per-feature gain; the gain is rounded to the I/O dtype first, as a stored
-//                  input current would be).
+//                  input current would be, and the backward multiplies by the same rounded
+//                  gain, the exact derivative of that input current).
 template <int IO, int V>
 struct DenseIn {
     using raw = typename IoVec<IO, V>::raw;
@@ -358,14 +366,10 @@ struct GainSpikeIn {
                                    std::conditional_t<SPK == SNN_SPK_U8 && V == 8, uint64_t, uint32_t>>;
     const uint8_t* s;
     int64_t row_bytes;
-    float gx[V];   // gain of the lane's neurons, rounded to the I/O dtype (forward input)
-    float gy[V];   // gain in fp32 (backward output)
+    float gx[V];   // gain of the lane's neurons, rounded to the I/O dtype
     __device__ void init(const float* gain, int64_t F, int64_t n0, bool active) {
 #pragma unroll
-        for (int j = 0; j < V; ++j) {
-            gy[j] = active ? gain[(n0 + j) % F] : 0.0f;
-            gx[j] = IO == SNN_IO_BF16 ? bf16_lo(pack_bf16x2(gy[j], 0.0f)) : gy[j];
-        }
+        for (int j = 0; j < V; ++j) gx[j] = io_round<IO>(active ? gain[(n0 + j) % F] : 0.0f);
     }
     __device__ raw load(int64_t N, int64_t t, int64_t n0) const {
         if constexpr (SPK == SNN_SPK_IO) {
@@ -603,7 +607,7 @@ __device__ __forceinline__ void backward_rows(const LifK& c, const In& in, const
                 else                          // k (1 - V_th delta^t)
                     dv_next = fmaf(-c.kth, d, c.k);
                 g[j] = fmaf(Io::get(gr[i], j), d, dv_next * g[j]);
-                if constexpr (GAIN) out[j] = in.gy[j] * g[j];
+                if constexpr (GAIN) out[j] = in.gx[j] * g[j];
                 else out[j] = g[j];
             }
             Io::store(gx, (t0 + i) * N + n0, out);
@@ -775,20 +779,16 @@ __global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64
 // layer's spikes, the checkpoints (all L membranes every K steps, saved[chunk][l][N]) and,
 // backward, the last layer's dL/dy and layer 0's dL/dx go through memory.  The gain is
 // rounded to the I/O dtype before it multiplies a spike, as a stored input current would
-// be; the gradient handed down a layer, gain dL/dx, stays in fp32.
+// be, and the gradient handed down a layer is that rounded gain times dL/dx, kept in fp32.
 template <int V, int L>
 struct StackGains {
-    float gx[L - 1][V];   // rounded to the I/O dtype (forward input)
-    float gy[L - 1][V];   // fp32 (gradient handed down)
+    float gx[L - 1][V];   // rounded to the I/O dtype
     template <int IO>
     __device__ void init(const float* gains, int64_t F, int64_t n0, bool active) {
 #pragma unroll
         for (int l = 0; l < L - 1; ++l) {
 #pragma unroll
-            for (int j = 0; j < V; ++j) {
-                gy[l][j] = active ? gains[l * F + (n0 + j) % F] : 0.0f;
-                gx[l][j] = IO == SNN_IO_BF16 ? bf16_lo(pack_bf16x2(gy[l][j], 0.0f)) : gy[l][j];
-            }
+            for (int j = 0; j < V; ++j) gx[l][j] = io_round<IO>(active ? gains[l * F + (n0 + j) % F] : 0.0f);
         }
     }
 };
@@ -949,7 +949,7 @@ __device__ __forceinline__ void stack_backward_chunk(const LifK& c, const DenseI
                     else                          // k (1 - V_th delta^t)
                         dv_next = fmaf(-c.kth, d, c.k);
                     g[l][j] = fmaf(gs, d, dv_next * g[l][j]);
-                    if (l > 0) gs = G.gy[l - 1][j] * g[l][j];
+                    if (l > 0) gs = G.gx[l - 1][j] * g[l][j];
                 }
                 out[j] = g[0][j];
             }
@@ -1085,9 +1085,9 @@ __global__ __launch_bounds__(kBlock) void gain_backward_kernel(int64_t T, int64_
     using Io = IoVec<IO, V>;
     const int64_t n0 = (xcd_contiguous_block() * kBlock + threadIdx.x) * V;
     if (n0 >= N) return;
-    float gv[V];
+    float gv[V];   // the gain as the forward applies it (rounded to the I/O dtype)
 #pragma unroll
-    for (int j = 0; j < V; ++j) gv[j] = gain[(n0 + j) % F];
+    for (int j = 0; j < V; ++j) gv[j] = io_round<IO>(gain[(n0 + j) % F]);
     auto emit = [&](const typename Io::raw& r, int64_t t) {
         float out[V];
 #pragma unroll
@@ -1225,9 +1225,9 @@ __global__ __launch_bounds__(kBlock) void gain_backward_flat_kernel(int64_t piec
     flat_pieces<W, typename Io::raw>(
         pieces, F, step, gain, [&](int64_t e) { return Io::load(gx_next, e); },
         [&](const typename Io::raw& r, const FlatGains<W>& g, int64_t e) {
-            float out[W];
+            float out[W];   // the gain as the forward applies it (rounded to the I/O dtype)
 #pragma unroll
-            for (int j = 0; j < W; ++j) out[j] = g.g[j] * Io::get(r, j);
+            for (int j = 0; j < W; ++j) out[j] = io_round<IO>(g.g[j]) * Io::get(r, j);
             Io::store(gs, e, out);
         });
 }

@@ -4,7 +4,8 @@
  * spikes, hard and soft reset, one and several chunks, ragged N) and compares them with
  * the CPU oracle (test infrastructure) on the same seeded inputs: spikes exactly (a
  * mismatch is forgiven only strictly within 1e-5 of V_th, and that neuron is then left
- * out), membranes bit for bit, dL/dx within rtol * bound (1e-5 fp32, 2e-2 bf16).  It also
+ * out), membranes bit for bit, dL/dx within the oracle's error budget: |gpu - ref| <=
+ * q |ref| + (1 + q) 1e-5 err, q = 2^-8 for bf16 storage and 0 for fp32.  It also
  * checks argument errors.  Exit status 0 when everything matches. */
 #include <hip/hip_runtime_api.h>
 
@@ -107,15 +108,12 @@ static int run_case(const layer_case *c, hipStream_t stream)
     lif_oracle_params p = {c->decay, c->v_th, c->v_reset, c->alpha, c->reset == SNN_RESET_SOFT};
     uint8_t *y_ref = malloc(TN);
     float *v_ref = malloc(TN * 4);
-    double *gsd = malloc(TN * 8), *gsm = malloc(TN * 8), *g_ref = malloc(TN * 8), *bound = malloc(TN * 8);
-    for (int64_t i = 0; i < TN; ++i) {
-        gsd[i] = gs[i];
-        gsm[i] = fabs((double)gs[i]);
-    }
+    double *gsd = malloc(TN * 8), *g_ref = malloc(TN * 8), *err = malloc(TN * 8);
+    for (int64_t i = 0; i < TN; ++i) gsd[i] = gs[i];
     lif_oracle_forward(&p, T, N, x, NULL, NULL, y_ref, v_ref);
-    lif_oracle_backward(&p, T, N, v_ref, y_ref, gsd, gsm, NULL, g_ref, bound);
+    lif_oracle_backward(&p, T, N, v_ref, y_ref, gsd, NULL, NULL, NULL, g_ref, err, NULL);
 
-    const double rtol = bf16 ? 2e-2 : 1e-5;
+    const double q = bf16 ? 1.0 / 256.0 : 0.0;
     int64_t hard = 0, forgiven = 0, v_bad = 0, g_bad = 0, ties = 0;
     uint8_t *excluded = calloc(N, 1);
     for (int64_t t = 0; t < T; ++t) {
@@ -138,7 +136,8 @@ static int run_case(const layer_case *c, hipStream_t stream)
     }
     for (int64_t i = 0; i < TN; ++i) {
         if (excluded[i % N]) continue;
-        if (!(fabs((double)gx[i] - g_ref[i]) <= rtol * bound[i] + 1e-30)) ++g_bad;
+        const double tol = q * fabs(g_ref[i]) + (1.0 + q) * 1e-5 * err[i] + 1e-30;
+        if (!(fabs((double)gx[i] - g_ref[i]) <= tol)) ++g_bad;
     }
     printf("T=%lld N=%lld %s %s %s: ties=%lld forgiven=%lld hard=%lld v_unequal=%lld grad_bad=%lld\n",
            (long long)T, (long long)N, c->reset == SNN_RESET_SOFT ? "soft" : "hard", bf16 ? "bf16" : "f32",
@@ -152,7 +151,7 @@ static int run_case(const layer_case *c, hipStream_t stream)
     if (dsaved) HIP_OK(hipFree(dsaved));
     HIP_OK(hipFree(dv));
     free(x), free(gs), free(x16), free(gs16), free(spk), free(v), free(gx), free(gx16);
-    free(y_ref), free(v_ref), free(gsd), free(gsm), free(g_ref), free(bound), free(excluded);
+    free(y_ref), free(v_ref), free(gsd), free(g_ref), free(err), free(excluded);
     return (hard || v_bad || g_bad) ? 1 : 0;
 }
 

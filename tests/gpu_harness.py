@@ -74,11 +74,12 @@ def gpu_layer(w: W.Workload, x: torch.Tensor, gs: torch.Tensor, *, v_out=True, i
     return spikes, v, gx
 
 
-def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None, gy_mag=None):
-    """Oracle on x_np/gs_np (columns `cols` of the full problem if given) vs GPU outputs."""
+def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None):
+    """Oracle on x_np/gs_np (columns `cols` of the full problem if given) vs GPU outputs.
+    Returns the report and the oracle's (y, v, Grad)."""
     p = oracle.Params.of(w.params)
     y_ref, v_ref = oracle.forward(p, x_np)
-    gx_ref, bound = oracle.backward(p, v_ref, y_ref, gs_np, gy_mag)
+    ref = oracle.backward(p, v_ref, y_ref, gs_np)
     if cols is not None and w.T * w.N > (1 << 31):
         # a layer too large to copy whole: gather the sampled columns on the device
         y_gpu, v_gpu, g_gpu = gather_columns(w, spikes, v, gx, cols)
@@ -91,9 +92,8 @@ def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None, gy_mag=Non
             v_gpu = None if v_gpu is None else v_gpu[:, cols]
             g_gpu = g_gpu[:, cols]
     rep = parity.compare_forward(y_gpu, y_ref, v_ref, w.params.v_th, v_gpu=v_gpu, rep=rep)
-    rtol = parity.RTOL_BF16 if w.io == "bf16" else parity.RTOL_F32
-    parity.compare_grad(g_gpu, gx_ref, bound, rtol, rep)
-    return rep, (y_ref, v_ref, gx_ref, bound)
+    parity.compare_grad(g_gpu, ref, w.io, rep)
+    return rep, (y_ref, v_ref, ref)
 
 
 def gather_columns(w: W.Workload, spikes, v, gx, cols: np.ndarray):
@@ -134,6 +134,12 @@ def synth_bf16(a: np.ndarray) -> np.ndarray:
     return synth.to_bf16_bits(a)
 
 
+def round_io(a: np.ndarray, io: str) -> np.ndarray:
+    """float32 values rounded to the I/O dtype (to nearest even for bf16), as float32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return parity.bf16_to_f32(synth.to_bf16_bits(a)) if io == "bf16" else a
+
+
 __all__ = ["DEV", "say", "cfg_of", "to_dev", "to_host_f32", "upload_rows", "sample_columns", "gpu_layer",
-           "compare_layer", "gather_columns", "check_full", "check_sampled", "synth_bf16", "layer", "native", "np", "torch", "W",
+           "compare_layer", "gather_columns", "check_full", "check_sampled", "synth_bf16", "round_io", "layer", "native", "np", "torch", "W",
            "oracle", "parity"]

@@ -35,10 +35,9 @@ def test_lif_layer_autograd(H, dtype, reset):
     torch.cuda.synchronize()
     P = H.oracle.Params.of(p)
     y_ref, v_ref = H.oracle.forward(P, x_np)
-    gx_ref, bound = H.oracle.backward(P, v_ref, y_ref, gs_np)
+    ref = H.oracle.backward(P, v_ref, y_ref, gs_np)
     rep = H.parity.compare_forward(H.to_host_f32(y.detach()).reshape(T, N).astype(np.uint8), y_ref, v_ref, p.v_th)
-    rtol = H.parity.RTOL_BF16 if dtype == "bf16" else H.parity.RTOL_F32
-    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, N), gx_ref, bound, rtol, rep)
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, N), ref, dtype, rep)
     assert rep.ok(), str(rep)
 
 
@@ -59,9 +58,9 @@ def test_two_layers_with_gain(H):
     torch.cuda.synchronize()
     P = H.oracle.Params.of(p)
     xs, ys, vs = H.oracle.stack_forward(P, x_np, [gain_np], B, F)
-    gxs, gms = H.oracle.stack_backward(P, ys, vs, gs_np, [gain_np], B, F)
+    refs = H.oracle.stack_backward(P, ys, vs, gs_np, [gain_np], B, F)
     rep = H.parity.compare_forward(H.to_host_f32(y2.detach()).reshape(T, -1).astype(np.uint8), ys[1], vs[1], p.v_th)
-    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), gxs[0], gms[0], H.parity.RTOL_F32, rep)
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), refs[0], "f32", rep)
     assert rep.ok(), str(rep)
 
 
@@ -82,7 +81,8 @@ def test_inside_sequential(H):
 def test_fused_stack_autograd(H, dtype):
     """LIFLayer -> GainLIF(gain_12) -> GainLIF(gain_23): three layers, the later two fed
     straight from spikes; the last layer's spikes and x.grad from torch's autograd against
-    the oracle run layer by layer (the gain rounded to the I/O dtype, as the kernels do)."""
+    the oracle's stack (the gain rounded to the I/O dtype in both directions, as the kernels
+    apply it; in bf16 the gradient each layer hands down is a bf16 tensor)."""
     torch = H.torch
     from paper_2408_00280_amd.autograd import GainLIF, LIFLayer
     T, B, F = 24, 6, 1000
@@ -99,24 +99,12 @@ def test_fused_stack_autograd(H, dtype):
     (y * H.to_dev(gs_np, dtype).view(T, B, F)).sum().backward()
     torch.cuda.synchronize()
 
-    def rnd(a):
-        return H.parity.bf16_to_f32(H.synth_bf16(a)) if dtype == "bf16" else a
     P = H.oracle.Params.of(p)
-    xs, ys, vs = [x_np], [], []
-    for l in range(3):
-        yl, vl = H.oracle.forward(P, xs[l])
-        ys.append(yl)
-        vs.append(vl)
-        if l < 2:
-            xs.append(rnd(H.oracle.gain_forward(yl, gains[l], B, F)))
-    gy, gym = gs_np.astype(np.float64), np.abs(gs_np.astype(np.float64))
-    for l in range(2, -1, -1):
-        gx, gm = H.oracle.backward(P, vs[l], ys[l], gy, gym)
-        if l > 0:
-            gy, gym = H.oracle.gain_backward(gx, gm, gains[l - 1], B, F)
+    gr = [H.round_io(g, dtype) for g in gains]
+    _, ys, vs = H.oracle.stack_forward(P, x_np, gr, B, F)
+    ref = H.oracle.stack_backward(P, ys, vs, gs_np, gr, B, F, rounded_handoff=dtype == "bf16")[0]
     rep = H.parity.compare_forward(H.to_host_f32(y.detach()).reshape(T, -1).astype(np.uint8), ys[2], vs[2], p.v_th)
-    rtol = H.parity.RTOL_BF16 if dtype == "bf16" else H.parity.RTOL_F32
-    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), gx, gm, rtol, rep)
+    H.parity.compare_grad(H.to_host_f32(x.grad).reshape(T, -1), ref, dtype, rep)
     H.say(f"fused stack autograd {dtype}: {rep}")
     assert rep.ok(), str(rep)
 

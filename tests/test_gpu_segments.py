@@ -104,12 +104,11 @@ def test_segment_from_arbitrary_state(H, reset, io):
 
     op = H.oracle.Params.of(w.params)
     y_ref, v_ref = H.oracle.forward(op, x_np, v_init=v_in, y_init=(v_in >= np.float32(1.0)).astype(np.uint8))
-    g_ref, bound = H.oracle.backward(op, v_ref, y_ref, gs_np, g_next=g_in)
+    ref = H.oracle.backward(op, v_ref, y_ref, gs_np, g_next=g_in)
     y_gpu = H.parity.unpack_spikes(spikes.cpu().numpy(), N, w.spk)
     rep = H.parity.compare_forward(y_gpu, y_ref, v_ref, 1.0, v_gpu=v.cpu().numpy())
-    rtol = H.parity.RTOL_BF16 if io == "bf16" else H.parity.RTOL_F32
-    H.parity.compare_grad(H.to_host_f32(gx), g_ref, bound, rtol, rep)
-    H.parity.compare_grad(g_out.cpu().numpy()[None, :], g_ref[:1], bound[:1], H.parity.RTOL_F32, rep)
+    H.parity.compare_grad(H.to_host_f32(gx), ref, io, rep)
+    H.parity.compare_grad(g_out.cpu().numpy()[None, :], ref.sel(slice(0, 1)), "f32", rep)
     assert rep.ok(), str(rep)
     assert np.array_equal(v_last.cpu().numpy().view(np.uint32), v_ref[-1].view(np.uint32))
 

@@ -3,7 +3,7 @@ layer whose input current gain[f] * spikes_in is formed inside the kernel from t
 previous layer's spikes.  Forward outputs are checked against the oracle (spikes exact,
 membranes bit for bit) and against the unfused pair on the GPU (gain kernel, then the
 dense layer: spikes, membranes and checkpoints bit for bit); the gradient passed to
-spikes_in is checked against the oracle's gain * dL/dx within rtol * bound."""
+spikes_in is checked against the oracle's gain * dL/dx within its error budgets."""
 import itertools
 
 import numpy as np
@@ -43,13 +43,10 @@ def _inputs(T, B, F, io, seed, rate=0.35):
     return y_in, gain, gs
 
 
-def _round_io(H, a: np.ndarray, io: str) -> np.ndarray:
-    return H.parity.bf16_to_f32(H.synth_bf16(a)) if io == "bf16" else a
-
-
 def _oracle_layer(H, cfg, y_in, gain, gs, io, cols=None):
     """Oracle of the gain-fed layer on all neurons, or on columns `cols` (each column keeps
-    its own feature's gain).  Returns (y, v, dL/d spikes_in, bound)."""
+    its own feature's gain).  The gain enters rounded to the I/O dtype, in both directions, as
+    the kernels apply it.  Returns (y, v, oracle.Grad of dL/d spikes_in)."""
     F = gain.size
     if cols is not None:
         y_in, gs = y_in[:, cols], gs[:, cols]
@@ -58,11 +55,9 @@ def _oracle_layer(H, cfg, y_in, gain, gs, io, cols=None):
     else:
         B = y_in.shape[1] // F
     p = H.oracle.Params.of(cfg)
-    x = _round_io(H, H.oracle.gain_forward(y_in, gain, B, F), io)
-    y_ref, v_ref = H.oracle.forward(p, x)
-    gx, gm = H.oracle.backward(p, v_ref, y_ref, gs)
-    gy, gym = H.oracle.gain_backward(gx, gm, gain, B, F)
-    return y_ref, v_ref, gy, gym
+    gain = H.round_io(gain, io)
+    y_ref, v_ref = H.oracle.forward(p, H.oracle.gain_forward(y_in, gain, B, F))
+    return y_ref, v_ref, H.oracle.gain_backward(H.oracle.backward(p, v_ref, y_ref, gs), gain, B, F)
 
 
 def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
@@ -70,7 +65,7 @@ def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
     N = B * F
     cfg = H.layer.LifConfig(0.5, 1.0, reset=reset, io=io, spk=spk)
     y_in, gain, gs = _inputs(T, B, F, io, seed)
-    gs = _round_io(H, gs, io)
+    gs = H.round_io(gs, io)
     s_in = (H.to_dev(y_in.astype(np.float32), io) if spk == "io"
             else torch.from_numpy(_pack(y_in, spk)).to(H.DEV))
     g_dev = torch.from_numpy(gain).to(H.DEV)
@@ -90,14 +85,13 @@ def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
     torch.cuda.synchronize()
 
     cols = None if n_sample is None else H.sample_columns(N, n_sample, seed=seed)
-    y_ref, v_ref, gy_ref, gy_bound = _oracle_layer(H, cfg, y_in, gain, gs, io, cols)
+    y_ref, v_ref, gy_ref = _oracle_layer(H, cfg, y_in, gain, gs, io, cols)
     y_gpu = H.parity.unpack_spikes(H.to_host_f32(spikes) if spk == "io" else spikes.cpu().numpy(), N, spk)
     v_gpu, g_gpu = v.cpu().numpy(), H.to_host_f32(g_in)
     if cols is not None:
         y_gpu, v_gpu, g_gpu = y_gpu[:, cols], v_gpu[:, cols], g_gpu[:, cols]
     rep = H.parity.compare_forward(y_gpu, y_ref, v_ref, cfg.v_th, v_gpu=v_gpu)
-    rtol = H.parity.RTOL_BF16 if io == "bf16" else H.parity.RTOL_F32
-    H.parity.compare_grad(g_gpu, gy_ref, gy_bound, rtol, rep)
+    H.parity.compare_grad(g_gpu, gy_ref, io, rep)
     return rep, y_ref
 
 
@@ -190,7 +184,7 @@ def test_workload_stack_fused(H, spk):
     assert all(s.x is None for s in states[1:])
     p = H.oracle.Params.of(w.params)
     xs, ys, vs = H.oracle.stack_forward(p, x_np, gains_np, B, F)
-    gxs, gms = H.oracle.stack_backward(p, ys, vs, gs_np, gains_np, B, F)
+    refs = H.oracle.stack_backward(p, ys, vs, gs_np, gains_np, B, F)
     rep = H.parity.Report()
     for l in range(w.layers):
         sp = states[l].spikes
@@ -199,9 +193,9 @@ def test_workload_stack_fused(H, spk):
                                      ys[l], vs[l], w.params.v_th, v_gpu=states[l].v.cpu().numpy())
         H.say(f"fused stack layer {l} ({spk}): rate {ys[l].mean():.3f} {r}")
         assert r.ok(), f"layer {l}: {r}"
-    H.parity.compare_grad(H.to_host_f32(grads[0]), gxs[0], gms[0], H.parity.RTOL_F32, rep)
+    H.parity.compare_grad(H.to_host_f32(grads[0]), refs[0], w.io, rep)
     for l in range(w.layers - 1):   # dL/dy of layer l = gain_l * dL/dx of layer l + 1
-        gy, gym = H.oracle.gain_backward(gxs[l + 1], gms[l + 1], gains_np[l], B, F)
-        H.parity.compare_grad(H.to_host_f32(grads[l + 1]), gy, gym, H.parity.RTOL_F32, rep)
+        gy = H.oracle.gain_backward(refs[l + 1], gains_np[l], B, F)
+        H.parity.compare_grad(H.to_host_f32(grads[l + 1]), gy, w.io, rep)
     H.say(f"fused stack gradients ({spk}): {rep}")
     assert rep.ok(), str(rep)

@@ -32,19 +32,41 @@ MUTANTS = {
     "surrogate_drops_alpha": ("return alpha * e / ((1.0 + e) * (1.0 + e));", "return e / ((1.0 + e) * (1.0 + e));"),
     "surrogate_not_squared": ("return alpha * e / ((1.0 + e) * (1.0 + e));", "return alpha * e / (1.0 + e);"),
     "reset_term_sign": ("(rest - k * vt) * d;", "(k * vt - rest) * d;"),
-    "reset_detached": ("dv_next = k * (1.0 - (double)y[i]) + (rest - k * vt) * d;",
-                       "dv_next = k * (1.0 - (double)y[i]);"),
-    "reset_gate_dropped": ("dv_next = k * (1.0 - (double)y[i]) + (rest - k * vt) * d;",
-                           "dv_next = k + (rest - k * vt) * d;"),
-    "soft_backward_sign": ("dv_next = k * (1.0 - th * d);", "dv_next = k * (1.0 + th * d);"),
-    "soft_backward_detached": ("dv_next = k * (1.0 - th * d);", "dv_next = k;"),
-    "recurrence_factor_k_only": ("const double g = gy[i] * d + dv_next * g_after;",
+    "reset_detached": ("D = k * (1.0 - (double)y[i]) + (rest - k * vt) * d;",
+                       "D = k * (1.0 - (double)y[i]);"),
+    "reset_gate_dropped": ("D = k * (1.0 - (double)y[i]) + (rest - k * vt) * d;",
+                           "D = k + (rest - k * vt) * d;"),
+    "soft_backward_sign": ("D = k * (1.0 - th * d);", "D = k * (1.0 + th * d);"),
+    "soft_backward_detached": ("D = k * (1.0 - th * d);", "D = k;"),
+    "recurrence_factor_k_only": ("const double g = gy[i] * d + D * g_after;",
                                  "const double g = gy[i] * d + k * g_after;"),
-    "direct_term_dropped": ("const double g = gy[i] * d + dv_next * g_after;",
-                            "const double g = gy[i] + dv_next * g_after;"),
+    "direct_term_dropped": ("const double g = gy[i] * d + D * g_after;",
+                            "const double g = gy[i] + D * g_after;"),
     "terminal_gradient_one": ("double g_after = g_next ? g_next[n] : 0.0;",
                               "double g_after = g_next ? g_next[n] : 1.0;"),
     "gain_glue_wrong_index": ("x_next[i] = gain[f] * (float)y[i];", "x_next[i] = gain[b % F] * (float)y[i];"),
+    # the stack of layers joined by a gain
+    "stack_forward_first_gain_everywhere": ("gains + l * F, xs + (l + 1) * TN);", "gains, xs + (l + 1) * TN);"),
+    "stack_forward_x_to_every_layer": ("lif_oracle_forward(p, T, B * F, xs + l * TN,",
+                                       "lif_oracle_forward(p, T, B * F, x,"),
+    "stack_backward_gain_of_other_layer": ("gains + l * F, h_g,", "gains + (L - 2 - l) * F, h_g,"),
+    "stack_backward_gain_index": ("const double a = (double)gain[f];", "const double a = (double)gain[b % F];"),
+    "stack_backward_gain_dropped": ("gy[i] = a * gx_next[i];", "gy[i] = gx_next[i];"),
+    "stack_backward_ignores_layer_above": ("lif_oracle_backward(p, T, N, v + o, y + o, h_g, h_err,",
+                                           "lif_oracle_backward(p, T, N, v + o, y + o, gy, h_err,"),
+    "stack_backward_budget_as_gradient": ("lif_oracle_gain_backward(T, B, F, gx + o + TN,",
+                                          "lif_oracle_gain_backward(T, B, F, gx_err + o + TN,"),
+    "stack_backward_layer0_membranes": ("lif_oracle_backward(p, T, N, v + o, y + o, h_g,",
+                                        "lif_oracle_backward(p, T, N, v, y, h_g,"),
+    # the error budgets
+    "budget_without_condition_number": ("const double dc = d * (1.0 + alpha * fabs(vt - th));",
+                                        "const double dc = d;"),
+    "budget_propagated_by_term_magnitudes": ("fabs(D) * e_after;", "m * e_after;"),
+    "budget_without_factor_rounding": ("+ m * fabs(g_after) +", "+"),
+    "budget_without_direct_term": ("fabs(gy[i]) * dc +", ""),
+    "budget_rounding_not_carried": ("const double r = (gy_rnd ? gy_rnd[i] * d : 0.0) + fabs(D) * r_after;",
+                                    "const double r = gy_rnd ? gy_rnd[i] * d : 0.0;"),
+    "budget_handoff_rounding_ignored": ("h_rnd[i] += fabs(h_g[i]);", "h_rnd[i] += 0.0;"),
 }
 
 

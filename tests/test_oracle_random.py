@@ -74,10 +74,10 @@ def test_temporal_split_random(lib, p, T, split, seed):
     x = rng.normal(0.6 * p.v_th, 0.5 * p.v_th + 0.1, size=(T, 9)).astype(np.float32)
     gy = rng.normal(size=(T, 9))
     y, v = oracle.forward(p, x, lib=lib)
-    g, _ = oracle.backward(p, v, y, gy, lib=lib)
+    g = oracle.backward(p, v, y, gy, lib=lib).g
     y1, v1 = oracle.forward(p, x[:a], lib=lib)
     y2, v2 = oracle.forward(p, x[a:], v_init=v1[-1], y_init=y1[-1], lib=lib)
     assert np.array_equal(np.vstack([y1, y2]), y) and np.array_equal(np.vstack([v1, v2]), v)
-    g2, _ = oracle.backward(p, v2, y2, gy[a:], lib=lib)
-    g1, _ = oracle.backward(p, v1, y1, gy[:a], g_next=g2[0], lib=lib)
+    g2 = oracle.backward(p, v2, y2, gy[a:], lib=lib).g
+    g1 = oracle.backward(p, v1, y1, gy[:a], g_next=g2[0], lib=lib).g
     assert np.array_equal(np.vstack([g1, g2]), g)
