@@ -6,7 +6,9 @@ x[T=16, B=64, C=128, H=32, W=32] (fp32 I/O, u8 spikes, decay 0.5, V_th 1, hard r
 sigmoid surrogate alpha = 4), with seeded synthetic inputs already resident in HBM.
 Prints ONE JSON line: neuron-timesteps/s over the timed steps, the HBM roofline of the
 dominant kernel (the backward) from HIP events recorded on the launch stream around every
-launch, and the CPU oracle's throughput on the host as a baseline.
+launch, a plain copy's bandwidth on the box, and -- after the timed region -- the timed
+step's outputs checked against the CPU oracle on sampled neurons and the oracle's own
+throughput on the host as a baseline (one core pinned, and all cores).
 
     python bench.py [--steps K] [--warmup W] [--workload conv|single|long|stack|large]
                     [--T T] [--fused-stack | --depth-stack] [--graph-trials N]
@@ -119,10 +121,63 @@ def _repeat(fn, min_s: float = 3.0):
             return dt / runs, runs
 
 
+def host_info() -> dict:
+    """The host CPU and the oracle's compiler and flags."""
+    import subprocess
+
+    import oracle
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    try:
+        gcc = subprocess.run(["gcc", "--version"], capture_output=True, text=True, timeout=30).stdout.splitlines()[0]
+    except (OSError, IndexError, subprocess.SubprocessError):
+        gcc = None
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "threads_allowed": host_threads(),
+            "oracle_compiler": gcc, "oracle_cflags": " ".join(oracle.CFLAGS)}
+
+
+def _pinned_single_core(p, x_np, gs_np, gains, F, reps: int = 3) -> dict:
+    """Forward and backward of the oracle timed separately on one thread pinned to one core
+    (sched_setaffinity on the calling thread), median of `reps` runs each."""
+    import numpy as np
+
+    import oracle
+    allowed = sorted(os.sched_getaffinity(0))
+    core = allowed[-1]
+    os.sched_setaffinity(0, {core})
+    try:
+        fwd, bwd = [], []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            if gains is None:
+                y, v = oracle.forward(p, x_np)
+            else:
+                B = x_np.shape[1] // F
+                _, ys, vs = oracle.stack_forward(p, x_np, gains, B, F)
+            t1 = time.perf_counter()
+            if gains is None:
+                oracle.backward(p, v, y, gs_np)
+            else:
+                oracle.stack_backward(p, ys, vs, gs_np, gains, B, F)
+            t2 = time.perf_counter()
+            fwd.append(t1 - t0)
+            bwd.append(t2 - t1)
+    finally:
+        os.sched_setaffinity(0, set(allowed))
+    return {"core": core, "pinned": "sched_setaffinity of the calling thread", "reps": reps,
+            "forward_s_median": float(np.median(fwd)), "backward_s_median": float(np.median(bwd)),
+            "forward_s": fwd, "backward_s": bwd}
+
+
 def cpu_baseline(w, x_np, gs_np, gains=None):
-    """The CPU oracle on the host: one thread over the sample, then the same oracle
-    functions on disjoint neuron slices, one thread per core (the slicing is harness code;
-    the oracle releases the interpreter lock inside its C calls)."""
+    """The CPU oracle on the host: one thread pinned to one core (forward and backward timed
+    separately), then the same oracle functions on disjoint neuron slices, one thread per
+    core (the slicing is harness code; the oracle releases the interpreter lock inside its
+    C calls)."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -132,7 +187,8 @@ def cpu_baseline(w, x_np, gs_np, gains=None):
     layers = 1 if gains is None else len(gains) + 1
     T, n = x_np.shape
     nts = layers * T * n
-    dt1, runs1 = _repeat(lambda: _oracle_pass(p, x_np, gs_np, gains, w.F))
+    one = _pinned_single_core(p, x_np, gs_np, gains, w.F)
+    dt1 = one["forward_s_median"] + one["backward_s_median"]
 
     cores = host_threads()
     unit = w.F if gains is not None else 1          # stack slices keep whole feature rows
@@ -146,7 +202,73 @@ def cpu_baseline(w, x_np, gs_np, gains=None):
     return {"value": nts / dtn, "unit": "neuron-timesteps/s", "cores": len(parts), "kind": "oracle",
             "sample": f"{layers} layer(s) x {T} steps x {n} neurons ({nts} nts, {what}), forward + backward, "
                       f"{len(parts)} threads on disjoint neuron slices, {runsn} run(s) of {dtn:.3f} s",
-            "single_thread": {"value": nts / dt1, "cores": 1, "seconds_per_run": dt1, "runs": runs1}}
+            "single_thread": {"value": nts / dt1, "cores": 1, "seconds_per_run": dt1,
+                              "forward_nts_per_s": nts / one["forward_s_median"],
+                              "backward_nts_per_s": nts / one["backward_s_median"], **one},
+            "host": host_info()}
+
+
+def sample_columns(N: int, n_sample: int = 4096, seed: int = 0):
+    """Neuron columns for the parity check: the first and last 1024, plus random ones."""
+    import numpy as np
+    if N <= n_sample:
+        return np.arange(N)
+    rng = np.random.default_rng(seed)
+    edge = np.r_[np.arange(1024), np.arange(N - 1024, N)]
+    inner = 1024 + rng.choice(N - 2048, size=n_sample - edge.size, replace=False)
+    return np.unique(np.r_[edge, inner])
+
+
+def parity_check(w, st, gains_np, schedule: str, cols) -> dict:
+    """The timed step's outputs (one buffer set, after the timed region) against the oracle
+    on sampled neuron columns: every stored layer's spikes exactly (near-threshold rule) and
+    the first layer's dL/dx within the oracle's error budgets (tests/parity.py)."""
+    import numpy as np
+
+    import oracle
+    from synth import workloads as W
+    from tests import gpu_harness, parity
+    L = w.layers
+    p = oracle.Params.of(w.params)
+    x, gs = W.x_cols(w, cols), W.gs_cols(w, cols)
+    rep = parity.Report()
+    if L == 1:
+        y_ref, v_ref = oracle.forward(p, x)
+        ys, vs = [y_ref], [v_ref]
+        ref = oracle.backward(p, v_ref, y_ref, gs)
+    else:
+        F = w.F
+        g_io = [gpu_harness.round_io(g[cols % F], w.io) for g in gains_np]
+        _, ys, vs = oracle.stack_forward(p, x, g_io, 1, cols.size)
+        ref = oracle.stack_backward(p, ys, vs, gs, g_io, 1, cols.size)[0]
+    stored = [L - 1] if schedule == "fused across depth" else list(range(L))
+    for l in stored:
+        y_gpu, _, _ = gpu_harness.gather_columns(w, st["spk"][l], None, st["g"][0], cols)
+        parity.compare_forward(y_gpu, ys[l], vs[l], w.params.v_th, rep=rep)
+    _, _, g_gpu = gpu_harness.gather_columns(w, st["spk"][0], None, st["g"][0], cols)
+    parity.compare_grad(g_gpu, ref, w.io, rep)
+    return {"ok": rep.ok(), "columns": int(cols.size), "layers_checked": stored, **rep.counts(),
+            "rule": "spikes exact unless the oracle membrane is strictly within 1e-5 of V_th; dL/dx within "
+                    "q|ref| + (1+q)(1e-5 err + 2^-8 rnd), q = 2^-8 for bf16 storage else 0"}
+
+
+def copy_ceiling(torch, dev, nbytes: int = 1 << 30, reps: int = 5) -> dict:
+    """A plain device-to-device copy of `nbytes`: the practical HBM ceiling on this machine."""
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b
+    return {"bytes_copied": nbytes, "ms": ms, "GB/s": 2 * nbytes / (ms * 1e-3) / 1e9,
+            "frac_of_peak": 2 * nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "note": "torch copy_ of 1 GiB, read + write bytes over event time"}
 
 
 def compare_serial(args):
@@ -495,7 +617,12 @@ def main():
     trials = args.graph_trials if args.graph_trials is not None else (1000 if w.name == "single" else 0)
     if trials and L == 1:
         out["graph_trials"] = graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev)
+    out["copy_ceiling"] = copy_ceiling(torch, dev)
     if not args.no_cpu_baseline:
+        # the oracle's leg, after the timed region: the timed step's outputs against the
+        # oracle on sampled columns, then the oracle's own throughput on the host
+        out["parity"] = parity_check(w, sets[(K - 1) % R], gains_np, out["config"]["schedule"],
+                                     sample_columns(N))
         if keep_host:
             x_np, gs_np = np.concatenate(host["x"]), np.concatenate(host["gs"])
         else:   # a bounded sample: the first neurons over all steps
@@ -503,6 +630,9 @@ def main():
             x_np, gs_np = W.x_cols(w, cols), W.gs_cols(w, cols)
         out["cpu_baseline"] = cpu_baseline(w, x_np, gs_np, gains_np if L > 1 else None)
     print(json.dumps(out), flush=True)
+    if "parity" in out and not out["parity"]["ok"]:
+        print("bench.py: the timed outputs do not match the oracle", file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

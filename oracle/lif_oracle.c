@@ -81,7 +81,8 @@ void lif_oracle_backward(const lif_oracle_params *p, int64_t T, int64_t N, const
             const int64_t i = t * N + n;
             const double vt = v[i];
             const double d = surrogate(alpha, vt - th);
-            const double dc = d * (1.0 + alpha * fabs(vt - th));
+            /* d alpha |u| -> 0 as |u| -> inf: an infinite membrane adds nothing (not 0 * inf) */
+            const double dc = d > 0.0 ? d * (1.0 + alpha * fabs(vt - th)) : 0.0;
             double D, m;
             if (p->soft_reset) {
                 D = k * (1.0 - th * d);

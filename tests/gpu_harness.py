@@ -77,6 +77,9 @@ def gpu_layer(w: W.Workload, x: torch.Tensor, gs: torch.Tensor, *, v_out=True, i
 def compare_layer(w, spikes, v, gx, x_np, gs_np, cols=None, rep=None):
     """Oracle on x_np/gs_np (columns `cols` of the full problem if given) vs GPU outputs.
     Returns the report and the oracle's (y, v, Grad)."""
+    for a, name in ((x_np, "x"), (gs_np, "dL/dy")):   # the oracle must see what the kernel reads
+        assert np.array_equal(round_io(a, w.io), np.asarray(a, dtype=np.float32), equal_nan=True), \
+            f"{name} is not exact in {w.io}: round it before uploading and before the oracle"
     p = oracle.Params.of(w.params)
     y_ref, v_ref = oracle.forward(p, x_np)
     ref = oracle.backward(p, v_ref, y_ref, gs_np)

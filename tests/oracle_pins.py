@@ -348,6 +348,16 @@ def pin_nonfinite(lib):
     assert y[:, 0].tolist() == [0, 0] and np.isnan(v[1, 0])
     assert y[:, 1].tolist() == [1, 0] and v[1, 1] == np.float32(0.25)
     assert y[:, 2].tolist() == [0, 0] and v[1, 2] == -np.inf
+    # the error budgets stay finite wherever the gradient is (an infinite membrane has
+    # delta = 0 and contributes nothing), in both reset modes
+    x = np.full((5, 6), 0.3, dtype=np.float32)
+    x[0, 0], x[1, 1], x[2, 2], x[0, 3] = np.nan, np.inf, -np.inf, np.inf
+    for soft in (False, True):
+        p = oracle.Params(0.5, 1.0, soft_reset=soft)
+        y, v = oracle.forward(p, x, lib=lib)
+        r = oracle.backward(p, v, y, np.ones((5, 6)), lib=lib)
+        fin = np.isfinite(r.g)
+        assert fin[:, 4:].all() and np.all(np.isfinite(r.err[fin])), (soft, r.g, r.err)
 
 
 # ----------------------------------------------------------------- stack pins

@@ -66,3 +66,24 @@ def test_source_hash_ignores_comments_only(tmp_path):
     assert bench.source_hash(str(tmp_path)) == before
     src.write_text("int f(int a) { return a + 2; }\n")
     assert bench.source_hash(str(tmp_path)) != before
+
+
+def test_host_info_and_sampling():
+    info = bench.host_info()
+    assert info["oracle_cflags"] and "-ffp-contract=off" in info["oracle_cflags"]
+    assert info["threads_allowed"] >= 1
+    cols = bench.sample_columns(1 << 20)
+    assert cols.size == 4096 and cols[0] == 0 and cols[-1] == (1 << 20) - 1
+    assert list(cols[:1024]) == list(range(1024)) and (cols[1:] > cols[:-1]).all()
+    assert list(bench.sample_columns(100)) == list(range(100))
+
+
+def test_pinned_single_core_oracle_timing():
+    """The pinned single-core leg times forward and backward separately and restores the
+    thread's core mask afterwards."""
+    import oracle
+    w = W.custom("tiny", 6, 300, W.HARD_05)
+    before = os.sched_getaffinity(0)
+    one = bench._pinned_single_core(oracle.Params.of(w.params), W.x_full(w), W.gs_full(w), None, w.F)
+    assert os.sched_getaffinity(0) == before
+    assert one["reps"] == 3 and len(one["forward_s"]) == 3 and one["backward_s_median"] > 0

@@ -59,8 +59,7 @@ MUTANTS = {
     "stack_backward_layer0_membranes": ("lif_oracle_backward(p, T, N, v + o, y + o, h_g,",
                                         "lif_oracle_backward(p, T, N, v, y, h_g,"),
     # the error budgets
-    "budget_without_condition_number": ("const double dc = d * (1.0 + alpha * fabs(vt - th));",
-                                        "const double dc = d;"),
+    "budget_without_condition_number": ("d * (1.0 + alpha * fabs(vt - th))", "d"),
     "budget_propagated_by_term_magnitudes": ("fabs(D) * e_after;", "m * e_after;"),
     "budget_without_factor_rounding": ("+ m * fabs(g_after) +", "+"),
     "budget_without_direct_term": ("fabs(gy[i]) * dc +", ""),
