@@ -112,12 +112,10 @@ static void check_plan(const snn_lif_cfg& c, int64_t T, int64_t N) {
     CHECK(p.vb == 1 || p.vb == 2 || p.vb == 4);
     CHECK(N % p.vb == 0 && N % p.vf == 0);             // lanes never straddle the row end
     CHECK(p.k == 4 || p.k == 8 || p.k == 16 || p.k == 32);
-    CHECK(p.blkf == kBlock || p.blkf == kSyncBlock || p.blkf == kSmallBlock);
-    CHECK(p.blkb == kBlock || p.blkb == kSyncBlock || p.blkb == kSmallBlock);
-    // the launchers take one-wave workgroups for single-chunk layers of 1 or 2 neurons a lane
-    if (p.blkf == kSmallBlock) CHECK(!p.pipe && T <= p.k && p.vf <= 2);
-    if (p.blkb == kSmallBlock) CHECK(!p.pipe && T <= p.k && p.vb <= 2);
+    CHECK(p.blkf == kBlock || p.blkf == kSyncBlock);
+    CHECK(p.blkb == kBlock || p.blkb == kSyncBlock);
     if (p.blkf == kSyncBlock) CHECK(!p.pipe && T > p.k);
+    if (p.blkb == kSyncBlock) CHECK(!p.pipe && T > p.k && p.vb == 2);
     CHECK(p.lanes * p.vf >= N);
     CHECK(p.row_bytes == spike_row_bytes(&c, N));
     if (c.spk == SNN_SPK_BITS) CHECK(p.lanes * p.vf >= p.row_bytes * 8);   // every spike word written
