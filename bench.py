@@ -242,10 +242,10 @@ def parity_check(w, st, gains_np, schedule: str, cols) -> dict:
         _, ys, vs = oracle.stack_forward(p, x, g_io, 1, cols.size)
         ref = oracle.stack_backward(p, ys, vs, gs, g_io, 1, cols.size)[0]
     stored = [L - 1] if schedule == "fused across depth" else list(range(L))
-    for l in stored:
-        y_gpu, _, _ = gpu_harness.gather_columns(w, st["spk"][l], None, st["g"][0], cols)
+    g_gpu = None
+    for l in stored:   # spikes the schedule stores, and the first layer's dL/dx
+        y_gpu, _, g_gpu = gpu_harness.gather_columns(w, st["spk"][l], None, st["g"][0], cols)
         parity.compare_forward(y_gpu, ys[l], vs[l], w.params.v_th, rep=rep)
-    _, _, g_gpu = gpu_harness.gather_columns(w, st["spk"][0], None, st["g"][0], cols)
     parity.compare_grad(g_gpu, ref, w.io, rep)
     return {"ok": rep.ok(), "columns": int(cols.size), "layers_checked": stored, **rep.counts(),
             "rule": "spikes exact unless the oracle membrane is strictly within 1e-5 of V_th; dL/dx within "
@@ -343,9 +343,16 @@ def compare_serial(args):
 def system_info(torch) -> dict:
     """The device and software the numbers were taken on."""
     props = torch.cuda.get_device_properties(0)
+    rocm = None
+    try:
+        with open(os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), ".info", "version")) as f:
+            rocm = f.read().strip()
+    except OSError:
+        pass
     return {"device": props.name, "arch": getattr(props, "gcnArchName", None),
             "compute_units": props.multi_processor_count, "hbm_bytes": props.total_memory,
-            "hip": torch.version.hip, "torch": torch.__version__}
+            "rocm": rocm, "hip_runtime": torch.version.hip, "torch": torch.__version__,
+            "library_built_with": "hipcc --offload-arch=gfx950 -O3 -ffp-contract=off, packed fp32 off"}
 
 
 def graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev):
