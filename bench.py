@@ -12,7 +12,13 @@ throughput on the host as a baseline (one core pinned, and all cores).
 
     python bench.py [--steps K] [--warmup W] [--workload conv|single|long|stack|large]
                     [--T T] [--fused-stack | --depth-stack] [--graph-trials N]
-                    [--no-cpu-baseline] [--with-copy] [--compare-serial [--Ts ...]]
+                    [--no-cpu-baseline] [--no-configs] [--config-steps K2] [--with-copy]
+                    [--compare-serial [--Ts ...]]
+
+The default run (the conv-shaped headline) then also measures every other workload --
+the single layer, the long layer, the stack in its three schedules, the large bf16 layer
+at T = 4, 16, 64 and 256 -- each with its own timed steps and sampled oracle check, and
+records them under "configs" in the same line (--no-configs skips them).
 
 --fused-stack runs a stack's layers after the first fed straight from the previous
 layer's spikes through the gain (no stored input current or dL/dx between layers);
@@ -415,7 +421,12 @@ def main():
     ap.add_argument("--graph-trials", type=int, default=None,
                     help="also time this many independent forward+backward trials replayed from one HIP "
                          "graph (default 1000 for the single workload, else off)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (the sampled parity check and the CPU baseline)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="default run only: skip measuring the other workloads after the headline")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed steps for each of the other workloads in the default run")
     ap.add_argument("--with-copy", action="store_true",
                     help="also run a plain 1 GiB device copy (counter calibration runs)")
     ap.add_argument("--compare-serial", action="store_true",
@@ -433,6 +444,55 @@ def main():
         compare_serial(args)
         return
 
+    out = measure(args)
+    headline = (args.workload == "conv" and args.T is None and not args.fused_stack and not args.depth_stack)
+    if headline and not args.no_configs:
+        out["configs"] = other_configs(args)
+    print(json.dumps(out), flush=True)
+    bad = [name for name, rec in [("headline", out)] + list(out.get("configs", {}).items())
+           if "parity" in rec and not rec["parity"]["ok"]]
+    if bad:
+        print(f"bench.py: the timed outputs do not match the oracle ({', '.join(bad)})", file=sys.stderr)
+        sys.exit(1)
+
+
+# The other workloads, measured after the headline in the same default run: each with its
+# own timed steps and sampled oracle check (no CPU baseline), so that one run records
+# every configuration.
+OTHER_CONFIGS = [
+    ("single", dict(workload="single")),
+    ("long", dict(workload="long")),
+    ("stack", dict(workload="stack")),
+    ("stack_fused_gain", dict(workload="stack", fused_stack=True)),
+    ("stack_fused_depth", dict(workload="stack", depth_stack=True)),
+    ("large_T4", dict(workload="large", T=4)),
+    ("large_T16", dict(workload="large", T=16)),
+    ("large_T64", dict(workload="large", T=64)),
+    ("large_T256", dict(workload="large", T=256)),
+]
+
+
+def other_configs(args) -> dict:
+    import torch
+    keep = ("value", "unit", "ms_per_step", "steps", "warmup", "dtype", "config", "hbm_fraction_step", "roofline",
+            "kernels", "parity", "graph_trials")
+    res = {}
+    for name, over in OTHER_CONFIGS:
+        a = argparse.Namespace(**vars(args))
+        a.workload, a.T, a.fused_stack, a.depth_stack = over["workload"], over.get("T"), False, False
+        a.fused_stack = over.get("fused_stack", False)
+        a.depth_stack = over.get("depth_stack", False)
+        a.steps, a.warmup, a.with_copy, a.parity_only = args.config_steps, 2, False, True
+        a.graph_trials = None
+        print(f"bench.py: {name}", file=sys.stderr, flush=True)
+        rec = measure(a)
+        res[name] = {k: rec[k] for k in keep if k in rec}
+        torch.cuda.empty_cache()
+    return res
+
+
+def measure(args) -> dict:
+    """One workload: warmup, timed steps, the record (and the oracle leg unless skipped)."""
     import numpy as np
     import torch
 
@@ -453,7 +513,8 @@ def main():
     B, F = (N // w.F, w.F)
 
     # seeded inputs, generated on the host in row chunks and copied to HBM
-    keep_host = not args.no_cpu_baseline and T * N <= (1 << 28)
+    parity_only = getattr(args, "parity_only", False)
+    keep_host = not args.no_cpu_baseline and not parity_only and T * N <= (1 << 28)
     x0 = torch.empty((T, N), dtype=dt, device=dev)
     gs0 = torch.empty((T, N), dtype=dt, device=dev)
     host = {"x": [], "gs": []}
@@ -624,22 +685,21 @@ def main():
     trials = args.graph_trials if args.graph_trials is not None else (1000 if w.name == "single" else 0)
     if trials and L == 1:
         out["graph_trials"] = graph_trials(c, T, N, x0, gs0, row, sbytes, trials, bpn, dev)
-    out["copy_ceiling"] = copy_ceiling(torch, dev)
+    if not parity_only:
+        out["copy_ceiling"] = copy_ceiling(torch, dev)
     if not args.no_cpu_baseline:
         # the oracle's leg, after the timed region: the timed step's outputs against the
         # oracle on sampled columns, then the oracle's own throughput on the host
         out["parity"] = parity_check(w, sets[(K - 1) % R], gains_np, out["config"]["schedule"],
                                      sample_columns(N))
+    if not args.no_cpu_baseline and not parity_only:
         if keep_host:
             x_np, gs_np = np.concatenate(host["x"]), np.concatenate(host["gs"])
         else:   # a bounded sample: the first neurons over all steps
             cols = np.arange(min(N, max(1 << 12, (1 << 28) // T)))
             x_np, gs_np = W.x_cols(w, cols), W.gs_cols(w, cols)
         out["cpu_baseline"] = cpu_baseline(w, x_np, gs_np, gains_np if L > 1 else None)
-    print(json.dumps(out), flush=True)
-    if "parity" in out and not out["parity"]["ok"]:
-        print("bench.py: the timed outputs do not match the oracle", file=sys.stderr)
-        sys.exit(1)
+    return out
 
 
 if __name__ == "__main__":

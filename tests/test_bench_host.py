@@ -87,3 +87,16 @@ def test_pinned_single_core_oracle_timing():
     one = bench._pinned_single_core(oracle.Params.of(w.params), W.x_full(w), W.gs_full(w), None, w.F)
     assert os.sched_getaffinity(0) == before
     assert one["reps"] == 3 and len(one["forward_s"]) == 3 and one["backward_s_median"] > 0
+
+
+def test_other_configs_are_workloads():
+    """The default run's extra configurations name real workloads and schedules."""
+    names = [n for n, _ in bench.OTHER_CONFIGS]
+    assert len(set(names)) == len(names)
+    for _, over in bench.OTHER_CONFIGS:
+        w = W.WORKLOADS[over["workload"]]
+        if "T" in over:
+            assert w.name == "large" and over["T"] in W.LARGE_T
+        if over.get("fused_stack") or over.get("depth_stack"):
+            assert w.layers > 1
+    assert {o.get("T") for _, o in bench.OTHER_CONFIGS if o["workload"] == "large"} == set(W.LARGE_T)
