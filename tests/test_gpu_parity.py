@@ -163,6 +163,17 @@ def test_workload_large(H, T):
     H.torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("T", [32, 256])
+def test_workload_paper_monolayer(H, T):
+    """The paper's single-GPU workload shape (Sec. 5.3): a monolayer of 1,000,000 neurons with
+    its hyper-parameters (Sec. 5.1: k_tau 0.2, V_th 0.3, V_rest 0, alpha 4), the time-step
+    sweep's ends; the oracle checks 2^14 neuron columns over all T."""
+    w = H.W.WORKLOADS["paper_monolayer"].with_T(T)
+    rep = H.check_sampled(w, 1 << 14)
+    H.say(f"paper monolayer T={T}: {rep}")
+    assert rep.ok(), str(rep)
+
+
 def test_max_neurons(H):
     """The largest layer the ABI accepts in one row: N = 2^31 - 1 (odd, so one neuron per
     lane: a grid of 2^31 lanes), three steps (a short chunk with a tail); sampled columns
