@@ -485,8 +485,13 @@ def other_configs(args) -> dict:
         a.steps, a.warmup, a.with_copy, a.parity_only = args.config_steps, 2, False, True
         a.graph_trials = None
         print(f"bench.py: {name}", file=sys.stderr, flush=True)
-        rec = measure(a)
-        res[name] = {k: rec[k] for k in keep if k in rec}
+        try:
+            rec = measure(a)
+        except Exception as e:   # recorded; the headline above stands on its own
+            res[name] = {"error": f"{type(e).__name__}: {e}"}
+            print(f"bench.py: {name} failed: {e}", file=sys.stderr, flush=True)
+        else:
+            res[name] = {k: rec[k] for k in keep if k in rec}
         torch.cuda.empty_cache()
     return res
 
