@@ -8,12 +8,14 @@ run draws the same cases) instead of the fixed sets the pins in oracle_pins.py u
   derived from the number of roundings per step, and fires identically until the fp64
   membrane first comes within that bound of the threshold;
 * splitting the sequence at any step and handing over (v, y) forward and dL/dv backward
-  reproduces the single run bit for bit (Sec. 3.2).
+  reproduces the single run bit for bit (Sec. 3.2);
+* finite differences through 2- and 3-layer stacks joined by random gains confirm the
+  oracle's stack backward for every layer.
 
 CPU only."""
 import numpy as np
 import pytest
-from hypothesis import HealthCheck, given, settings
+from hypothesis import HealthCheck, assume, given, settings
 from hypothesis import strategies as st
 
 import oracle
@@ -81,3 +83,21 @@ def test_temporal_split_random(lib, p, T, split, seed):
     g2 = oracle.backward(p, v2, y2, gy[a:], lib=lib).g
     g1 = oracle.backward(p, v1, y1, gy[:a], g_next=g2[0], lib=lib).g
     assert np.array_equal(np.vstack([g1, g2]), g)
+
+
+@SETTINGS
+@given(p=PARAMS, L=st.integers(2, 3), T=st.integers(1, 5), B=st.integers(1, 2), F=st.integers(1, 3),
+       seed=st.integers(0, 2 ** 31 - 1))
+def test_fd_stack_random_params(lib, p, L, T, B, F, seed):
+    """Finite differences through a stack of L layers joined by random per-feature gains
+    (either sign) confirm every layer's dL/dx of the oracle's stack, as pin_fd_stack does for
+    fixed hyper-parameters."""
+    rng = np.random.default_rng(seed)
+    for _ in range(40):   # inputs whose fp64 trajectories stay clear of V_th in every layer
+        x = rng.normal(p.v_th * 0.7, abs(p.v_th) * 0.6 + 0.2, size=(T, B * F)).astype(np.float32)
+        gains = [rng.uniform(-0.8, 2.2, size=F).astype(np.float32) for _ in range(L - 1)]
+        if all(np.all(np.abs(v - p.v_th) > 2e-3) for v, _ in P._smooth_stack(p, x, gains, B)):
+            break
+    else:
+        assume(False)
+    P._stack_fd_case(lib, p, x, gains, B, F, rng.normal(size=(T, B * F)))
