@@ -185,3 +185,38 @@ def test_random_segments_equal_whole(H, case):
     H.say(f"random segments {i}: T={T} N={N} {lens} {reset} {io} {spk}: equal")
     del x, gs, spikes, saved, v, gx, states
     torch.cuda.empty_cache()
+
+
+def test_large_layer_as_segments_full_size(H):
+    """The large bf16 layer at its full size (T = 256, N = 2^24, bit spikes): eight chained
+    32-step segment calls give the single fused call's spikes and dL/dx bit for bit (the
+    segments run single-chunk plans in 256-lane workgroups, the fused call the long-walk
+    plan in 1024-lane workgroups)."""
+    torch = H.torch
+    T, N, S = 256, 1 << 24, 32
+    cfg = H.layer.LifConfig(0.5, 1.0, io="bf16", spk="bits")
+    c = cfg.c()
+    gen = torch.Generator(device=H.DEV)
+    gen.manual_seed(11)
+    x = (torch.randn((T, N), device=H.DEV, generator=gen) * 0.5 + 0.5).to(torch.bfloat16)
+    gs = torch.randn((T, N), device=H.DEV, generator=gen).to(torch.bfloat16)
+    spikes, saved, _ = H.layer.forward(cfg, x)
+    gx = H.layer.backward(cfg, x, saved, gs)
+    torch.cuda.synchronize()
+    del saved
+    seg_spikes = torch.empty_like(spikes)
+    seg_gx = torch.empty_like(gx)
+    v_last = torch.empty((T // S, N), dtype=torch.float32, device=H.DEV)
+    g = [torch.empty(N, dtype=torch.float32, device=H.DEV) for _ in range(2)]
+    assert H.native.snn_lif_saved_bytes(c, S, N) == 0
+    for s in range(T // S):
+        H.native.snn_lif_forward_seg(c, S, N, x[s * S], v_last[s - 1] if s else None, seg_spikes[s * S], None,
+                                     v_last[s], None)
+    for i, s in enumerate(range(T // S - 1, -1, -1)):
+        H.native.snn_lif_backward_seg(c, S, N, x[s * S], v_last[s - 1] if s else None, None, gs[s * S],
+                                      g[i % 2] if i else None, seg_gx[s * S], g[(i + 1) % 2])
+    torch.cuda.synchronize()
+    assert torch.equal(seg_spikes, spikes)
+    assert torch.equal(seg_gx.view(torch.int16), gx.view(torch.int16))
+    del x, gs, gx, seg_gx, spikes, seg_spikes
+    torch.cuda.empty_cache()
