@@ -1,6 +1,8 @@
 """The library driven from plain C (tests/c_abi/abi_check.c): hipMalloc'd memory, its own
-hipStream_t, the C ABI only.  The program compares five layers with the oracle and checks
-argument errors; it exits 0 when everything matches."""
+hipStream_t, the C ABI only.  The program compares five layers and two stacks fused across
+depth with the oracle, checks that sequences run as segments with the state handoff equal
+the single call bit for bit, and checks argument errors; it exits 0 when everything
+matches."""
 import os
 import subprocess
 
