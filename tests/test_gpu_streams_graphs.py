@@ -3,8 +3,9 @@
 It launches only on the caller's stream, allocates nothing and keeps no state between
 calls, so (a) a forward+backward captured into a HIP graph must reproduce the eager
 results on every replay, with other work and synchronizations between replays and the
-outputs overwritten before each, and (b) layers launched on two streams at once must give
-the same bits as the same layers run one after the other."""
+outputs overwritten before each (single layers, stacks fused across depth and gain-fed
+layers), and (b) layers launched on two streams at once must give the same bits as the
+same layers run one after the other."""
 import numpy as np
 import pytest
 
@@ -104,3 +105,54 @@ def test_two_streams_concurrently(H):
         for a, b in zip(got, ref):
             assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
     assert np.isfinite(H.to_host_f32(A[4])).all()
+
+
+STACK_CASES = [
+    # (schedule, L, reset, io, spk): fused across depth (2 or 3 layers) and the gain-fed layer
+    # of a stack fused across its gain; 40 steps = two 16-step chunks and a tail
+    ("depth", 3, "hard", "f32", "u8"),
+    ("depth", 2, "soft", "bf16", "bits"),
+    ("gain", 2, "hard", "f32", "u8"),
+    ("gain", 2, "soft", "bf16", "io"),
+]
+
+
+@pytest.mark.parametrize("schedule,L,reset,io,spk", STACK_CASES, ids=lambda v: str(v))
+def test_graph_replays_stack(H, schedule, L, reset, io, spk):
+    """The stack kernels captured into a HIP graph: every replay equals the eager run."""
+    torch = H.torch
+    T, B, F = 40, 6, 1000
+    N = B * F
+    cfg = H.layer.LifConfig(0.5, 1.0, reset=reset, io=io, spk=spk)
+    gen = torch.Generator(device=H.DEV)
+    gen.manual_seed(L * 100 + T)
+    x = (torch.randn((T, N), device=H.DEV, generator=gen) * 0.6 + 0.5).to(cfg.dtype)
+    gs = torch.randn((T, N), device=H.DEV, generator=gen).to(cfg.dtype)
+    gains = (torch.rand((L - 1, F), device=H.DEV, generator=gen) * 1.5 + 0.5).contiguous()
+    if schedule == "gain":
+        spikes_in, _, _ = H.layer.forward(cfg, x)        # a first layer's spikes feed the gain
+
+        def run():
+            spikes, saved, _ = H.layer.forward_gain(cfg, spikes_in, gains[0], B, F)
+            return [spikes, saved, H.layer.backward_gain(cfg, spikes_in, gains[0], saved, gs, B, F)]
+    else:
+        def run():
+            spikes, _, saved, _ = H.layer.stack_forward(cfg, x, gains, B, F)
+            return [spikes, saved, H.layer.stack_backward(cfg, x, gains, saved, gs, B, F)]
+
+    ref = [t.clone() for t in run()]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        outs = run()
+    for rep in range(3):
+        for t in outs:                   # poison every output between replays (eager fills)
+            if t.numel():
+                t.view(torch.uint8).fill_(0xA5)
+        junk = torch.randn(1 << 20, device=H.DEV).sum()   # unrelated eager work
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs, ref):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {rep} differs from eager"
+        del junk
