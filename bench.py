@@ -618,12 +618,14 @@ def measure(args) -> dict:
     torch.cuda.synchronize()
 
     K = args.steps
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range((n_launch + 1) * K)]
+    # one event before the first launch and one after every launch: launch j of step i runs
+    # between events i*n_launch + j and the next one
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_launch * K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    ev[0].record(stream)
     for i in range(K):
-        base = i * (n_launch + 1)
-        ev[base].record(stream)
+        base = i * n_launch
         for j, (_, _, f) in enumerate(plans[i % R]):
             f()
             ev[base + j + 1].record(stream)
@@ -632,7 +634,7 @@ def measure(args) -> dict:
 
     per = {}
     for i in range(K):
-        base = i * (n_launch + 1)
+        base = i * n_launch
         for j, (name, nbytes, _) in enumerate(plans[0]):
             d = per.setdefault(name, {"ms": [], "bytes": nbytes})
             d["ms"].append(ev[base + j].elapsed_time(ev[base + j + 1]))
