@@ -117,10 +117,16 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     return p;
 }
 
-// A stack of L layers fused across depth (lif_stack_*_kernel): 2 neurons per lane (1 when
-// N is odd), 16-step chunks -- L membranes per neuron and step in the backward's VGPRs --
-// or the shortest of kShortChunks that holds a short layer.
+// A stack of L layers fused across depth (lif_stack_*_kernel): 16-step chunks -- L
+// membranes per neuron and step in the backward's VGPRs -- or the shortest of kShortChunks
+// that holds a short layer.  One neuron per lane on layers of up to kStackNarrowN neurons:
+// the 3-layer backward then needs 77 VGPRs instead of 151, twice the waves hide the
+// latency of its load-then-compute chunks, and it ran 5-13% faster than with 2 neurons per
+// lane at 2^18-2^20 neurons (x[32][B*4096], B = 64-256; 2 layers 2-7%; below 2^18 the two
+// are within the run-to-run spread); beyond that the 8-byte rows of 2 neurons per lane (1
+// when N is odd) are as fast or faster (B = 768-2048).
 constexpr int kMaxStackLayers = 3;
+constexpr int64_t kStackNarrowN = 4 * kFillLanes;
 
 struct StackPlan {
     int v;
@@ -131,7 +137,7 @@ struct StackPlan {
 
 inline StackPlan make_stack_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     StackPlan p;
-    p.v = N % 2 != 0 ? 1 : 2;
+    p.v = N % 2 != 0 || N <= kStackNarrowN ? 1 : 2;
     p.k = 16;
     for (int k : kShortChunks) {
         if (T <= k && k < p.k) {
