@@ -97,10 +97,10 @@ def test_depth_stack_small(H, T, B, F, L, reset, io, spk):
 
 
 # the stack workload's shape (one neuron per lane), plus larger layers checked on sampled
-# columns: 2 neurons per lane beyond 2^20 neurons, 1 on odd layers, several chunks with a
-# tail, short single chunks
+# columns: 2 neurons per lane beyond 2^20 neurons (the first even size past it included), 1
+# on odd layers and up to 2^20, several chunks with a tail, short single chunks
 PLANS = [(32, 128, 4096, None), (40, 512, 4096, 1 << 12), (40, 3, 349525, 1 << 12), (4, 512, 4096, 1 << 12),
-         (9, 1, (1 << 20) + 1, 1 << 12), (33, 256, 4096, 1 << 12)]
+         (9, 1, (1 << 20) + 1, 1 << 12), (33, 256, 4096, 1 << 12), (17, 2, (1 << 19) + 1, 1 << 12)]
 
 
 @pytest.mark.parametrize("T,B,F,n_sample", PLANS, ids=lambda v: str(v))
