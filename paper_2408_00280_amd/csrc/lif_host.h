@@ -117,6 +117,21 @@ inline Plan make_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
     return p;
 }
 
+// The layer fed by the previous layer's spikes reads one spike word per lane and row (2-8
+// bytes) where the dense layer reads an I/O row of 8-16 bytes, so double-buffering its
+// chunks costs more in occupancy than it hides (fp32 backward: 191 instead of 79 VGPRs, 2
+// instead of 6 waves per SIMD; forward 127 instead of 69).  Its chunks are single-buffered
+// at the dense layer's chunk length, so the checkpoint layout and snn_lif_saved_bytes stay
+// the dense layer's.  At N = 2^19 (event timing, three alternating rounds): fp32 u8 spikes,
+// T = 32: forward 10.2 instead of 10.5 us, backward 29.7-29.9 instead of 30.7-31.0 us; bf16
+// bit spikes, T = 32: 11.1 instead of 11.8 us and 18.6 instead of 19.6-19.8 us; bf16 u8,
+// T = 64: backward 32.8 instead of 35.7-36.0 us, forward within 1%.
+inline Plan make_gain_plan(const snn_lif_cfg* c, int64_t T, int64_t N) {
+    Plan p = make_plan(c, T, N);
+    p.pipe = false;
+    return p;
+}
+
 // A stack of L layers fused across depth (lif_stack_*_kernel): 16-step chunks -- L
 // membranes per neuron and step in the backward's VGPRs -- or the shortest of kShortChunks
 // that holds a short layer.  One neuron per lane on layers of up to kStackNarrowN neurons:

@@ -151,7 +151,7 @@ snn_status snn_lif_forward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, in
     if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
     const int64_t N = B * F;
     if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, T, N);
+    const Plan p = make_gain_plan(cfg, T, N);
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (spikes_in == nullptr || gain == nullptr || spikes == nullptr || (need_saved && saved == nullptr))
         return SNN_E_NULL;
@@ -186,7 +186,7 @@ snn_status snn_lif_backward_gain(const snn_lif_cfg* cfg, int64_t T, int64_t B, i
     if ((st = check_gain_shape(T, B, F)) != SNN_OK) return st;
     const int64_t N = B * F;
     if (T == 0 || N == 0) return SNN_OK;
-    const Plan p = make_plan(cfg, T, N);
+    const Plan p = make_gain_plan(cfg, T, N);
     const bool need_saved = saved_bytes(p, T, N) > 0;
     if (spikes_in == nullptr || gain == nullptr || grad_s == nullptr || grad_s_in == nullptr ||
         (need_saved && saved == nullptr))

@@ -1,5 +1,5 @@
 // Host-only driver for AddressSanitizer / UndefinedBehaviorSanitizer runs, built with g++
-// (no GPU code): the library's argument checks and lane/chunk planner (lif_host.h), and the
+// (no GPU code): the library's argument checks and lane/chunk planners (lif_host.h), and the
 // CPU oracle (oracle/lif_oracle.c, built with gcc beside it).  Every plan the planner can
 // return must map to an instantiated kernel variant, cover every neuron and size its
 // checkpoint buffer without overflow; the oracle runs on ragged, empty and non-finite
@@ -133,6 +133,21 @@ static void check_plan(const snn_lif_cfg& c, int64_t T, int64_t N) {
     if (fs != SNN_OK || bs != SNN_OK)
         std::fprintf(stderr, "no kernel variant: io %d T %lld N %lld vf %d vb %d k %d pipe %d\n", c.io,
                      (long long)T, (long long)N, p.vf, p.vb, p.k, int(p.pipe));
+    CHECK(fs == SNN_OK && bs == SNN_OK);
+    // the gain-fed layer: single-buffered chunks of the same length, so the same checkpoints
+    const Plan gp = make_gain_plan(&c, T, N);
+    CHECK(!gp.pipe && gp.k == p.k && gp.vf == p.vf && gp.vb == p.vb && gp.lanes == p.lanes);
+    CHECK(saved_bytes(gp, T, N) == saved_bytes(p, T, N));
+    if (c.io == SNN_IO_F32) {
+        fs = forward_variant<SNN_IO_F32>(gp, Probe{});
+        bs = backward_variant<SNN_IO_F32>(gp, Probe{});
+    } else {
+        fs = forward_variant<SNN_IO_BF16>(gp, Probe{});
+        bs = backward_variant<SNN_IO_BF16>(gp, Probe{});
+    }
+    if (fs != SNN_OK || bs != SNN_OK)
+        std::fprintf(stderr, "no gain-fed kernel variant: io %d T %lld N %lld vf %d vb %d k %d\n", c.io,
+                     (long long)T, (long long)N, gp.vf, gp.vb, gp.k);
     CHECK(fs == SNN_OK && bs == SNN_OK);
     const StackPlan s = make_stack_plan(&c, T, N);
     CHECK((s.v == 1 || s.v == 2) && N % s.v == 0);
