@@ -3,7 +3,8 @@ layer whose input current gain[f] * spikes_in is formed inside the kernel from t
 previous layer's spikes.  Forward outputs are checked against the oracle (spikes exact,
 membranes bit for bit) and against the unfused pair on the GPU (gain kernel, then the
 dense layer: spikes, membranes and checkpoints bit for bit); the gradient passed to
-spikes_in is checked against the oracle's gain * dL/dx within its error budgets."""
+spikes_in is checked against the oracle's gain * dL/dx within its error budgets.  Fixed
+shapes at every lane/chunk plan, plus seeded random shapes, formats and hyper-parameters."""
 import itertools
 
 import numpy as np
@@ -60,10 +61,11 @@ def _oracle_layer(H, cfg, y_in, gain, gs, io, cols=None):
     return y_ref, v_ref, H.oracle.gain_backward(H.oracle.backward(p, v_ref, y_ref, gs), gain, B, F)
 
 
-def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False):
+def _run(H, T, B, F, reset, io, spk, seed, n_sample=None, inplace=False, params=(0.5, 1.0, 0.0, 4.0)):
     torch = H.torch
     N = B * F
-    cfg = H.layer.LifConfig(0.5, 1.0, reset=reset, io=io, spk=spk)
+    decay, v_th, v_reset, alpha = params
+    cfg = H.layer.LifConfig(decay, v_th, v_reset, alpha, reset=reset, io=io, spk=spk)
     y_in, gain, gs = _inputs(T, B, F, io, seed)
     gs = H.round_io(gs, io)
     s_in = (H.to_dev(y_in.astype(np.float32), io) if spk == "io"
@@ -126,6 +128,29 @@ def test_gain_layer_plans(H, T, B, F, reset, io, spk):
     rep, _ = _run(H, T, B, F, reset, io, spk, seed=7 * T + F, n_sample=1 << 12)
     assert rep.ok(), str(rep)
     H.torch.cuda.empty_cache()
+
+
+def _random_cases():
+    """Seeded random shapes (one chunk or several, a tail, 1 or 2 neurons per lane), formats
+    and hyper-parameters (decay in [0, 1], threshold, reset value, surrogate sharpness)."""
+    rng = np.random.default_rng(20240805)
+    out = []
+    for i in range(16):
+        T = int(rng.integers(1, 81))
+        B = int(rng.integers(1, 9))
+        F = int(rng.integers(1, 5000))
+        params = (float(rng.uniform(0, 1)), float(rng.uniform(0.2, 2.0)),
+                  float(rng.choice([0.0, rng.uniform(-0.5, 0.5)])), float(rng.uniform(1.0, 8.0)))
+        out.append((i, T, B, F, params, str(rng.choice(["hard", "soft"])), str(rng.choice(["f32", "bf16"])),
+                    str(rng.choice(["u8", "bits", "io"]))))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: f"rnd{c[0]}")
+def test_gain_layer_random(H, case):
+    i, T, B, F, params, reset, io, spk = case
+    rep, _ = _run(H, T, B, F, reset, io, spk, seed=3000 + i, params=params)
+    assert rep.ok(), f"{case}: {rep}"
 
 
 def test_gain_layer_in_place(H):
