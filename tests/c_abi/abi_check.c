@@ -386,6 +386,8 @@ int main(void)
     for (size_t i = 0; i < sizeof cases / sizeof cases[0]; ++i) fails += run_case(&cases[i], stream);
     fails += run_stack_case(3, 32, 6, 1000, SNN_RESET_HARD, SNN_IO_F32, SNN_SPK_U8, 21, stream);
     fails += run_stack_case(2, 40, 3, 4097, SNN_RESET_SOFT, SNN_IO_BF16, SNN_SPK_BITS, 22, stream);
+    /* past 2^20 neurons the stack takes 2 neurons per lane (one below): N = 2^20 + 2 */
+    fails += run_stack_case(2, 17, 2, 524289, SNN_RESET_SOFT, SNN_IO_F32, SNN_SPK_U8, 23, stream);
     const int64_t cuts_a[] = {1, 31, 32, 16}, cuts_b[] = {64, 16, 17};
     /* segment starts must stay 16-byte aligned: N = 64 * 1564, whose fp32 rows (400384 B) and
      * bit-spike rows (12512 B) are multiples of 16 bytes */
