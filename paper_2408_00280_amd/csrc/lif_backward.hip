@@ -63,9 +63,12 @@ snn_status backward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t 
         return backward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
-            constexpr bool Pc = decltype(PIPE)::value;
-            return launch(lif_backward_gain_kernel<IO, SPK, R, Vc, Kc, Pc>, grid_for((N + Vc - 1) / Vc), s, k, T, N,
-                          F, si, gain, p.row_bytes, sv, gs, gs_in);
+            if constexpr (decltype(PIPE)::value) {
+                return SNN_E_UNSUPPORTED;   // the gain-fed layer's plan never double-buffers
+            } else {
+                return launch(lif_backward_gain_kernel<IO, SPK, R, Vc, Kc>, grid_for((N + Vc - 1) / Vc), s, k,
+                              T, N, F, si, gain, p.row_bytes, sv, gs, gs_in);
+            }
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});

@@ -63,12 +63,15 @@ snn_status forward_gain_entry(int reset, const Plan& p, const LifK& k, int64_t T
         return forward_variant<IO>(p, [&](auto V, auto K, auto PIPE) {
             constexpr int R = decltype(rst)::value;
             constexpr int Vc = decltype(V)::value, Kc = decltype(K)::value;
-            constexpr bool Pc = decltype(PIPE)::value;
-            constexpr int FB = forward_batch(IO, Vc, Kc, Pc);
-            return v_out ? launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, true, Pc>, g, s, k, T, N, F, si, gain,
-                                  sp, p.row_bytes, sv, v_out)
-                         : launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, false, Pc>, g, s, k, T, N, F, si, gain,
-                                  sp, p.row_bytes, sv, v_out);
+            if constexpr (decltype(PIPE)::value) {
+                return SNN_E_UNSUPPORTED;   // the gain-fed layer's plan never double-buffers
+            } else {
+                constexpr int FB = forward_batch(IO, Vc, Kc, false);
+                return v_out ? launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, true>, g, s, k, T, N, F, si,
+                                      gain, sp, p.row_bytes, sv, v_out)
+                             : launch(lif_forward_gain_kernel<IO, SPK, R, Vc, FB, Kc, false>, g, s, k, T, N, F,
+                                      si, gain, sp, p.row_bytes, sv, v_out);
+            }
         });
     };
     return reset == SNN_RESET_SOFT ? go(IntC<SNN_RESET_SOFT>{}) : go(IntC<SNN_RESET_HARD>{});

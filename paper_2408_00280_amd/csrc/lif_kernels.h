@@ -548,7 +548,9 @@ __global__ __launch_bounds__(BLK) void lif_forward_kernel(LifK c, int64_t T, int
 
 // The same forward with the input current read from the previous layer's spikes through
 // the per-feature gain (neuron n has feature n % F).  Spikes in and out share the format.
-template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT, bool PIPE>
+// Its chunks are single-buffered: a spike word per lane and row is too little to hide
+// behind a second buffer's registers.
+template <int IO, int SPK, int RESET, int V, int K, int KC, bool VOUT>
 __global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_t T, int64_t N, int64_t F,
                                                                   const uint8_t* __restrict__ spikes_in,
                                                                   const float* __restrict__ gain,
@@ -563,10 +565,10 @@ __global__ __launch_bounds__(kBlock) void lif_forward_gain_kernel(LifK c, int64_
     in.row_bytes = row_bytes;
     in.init(gain, F, n0, n0 < N);
     if (first + kBlock * V <= N)
-        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, false, true>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                               nullptr, nullptr);
     else
-        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, PIPE, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
+        forward_lanes<IO, SPK, RESET, V, K, KC, VOUT, false, false>(c, in, T, N, n0, spikes, row_bytes, saved, v_out,
                                                                nullptr, nullptr);
 }
 
@@ -754,8 +756,8 @@ __global__ __launch_bounds__(BLK) void lif_backward_kernel(LifK c, int64_t T, in
 }
 
 // Backward of the gain-fed layer: recomputes from the previous layer's spikes and writes
-// gain[f] * dL/dx, the gradient with respect to those spikes.
-template <int IO, int SPK, int RESET, int V, int K, bool PIPE>
+// gain[f] * dL/dx, the gradient with respect to those spikes (single-buffered chunks).
+template <int IO, int SPK, int RESET, int V, int K>
 __global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64_t T, int64_t N, int64_t F,
                                                                    const uint8_t* __restrict__ spikes_in,
                                                                    const float* __restrict__ gain,
@@ -769,7 +771,7 @@ __global__ __launch_bounds__(kBlock) void lif_backward_gain_kernel(LifK c, int64
     in.s = spikes_in;
     in.row_bytes = row_bytes;
     in.init(gain, F, n0, true);
-    backward_lanes<IO, RESET, V, K, PIPE, true>(c, in, T, N, n0, saved, gs, gs_in, BwdSeg{nullptr, nullptr, nullptr});
+    backward_lanes<IO, RESET, V, K, false, true>(c, in, T, N, n0, saved, gs, gs_in, BwdSeg{nullptr, nullptr, nullptr});
 }
 
 // ------------------------------------------------------------------------------------
